@@ -1,0 +1,263 @@
+"""Seeded synthetic decode-attention workloads.
+
+This module draws inputs and nothing else: random normals, the bf16 cast,
+context lengths, page pools and block tables. It holds none of the attention
+arithmetic, so both the CPU oracle's tests and the GPU path's tests and bench
+can consume it without sharing any of the method's computation.
+
+Shapes follow the paper's statement of the decode problem (Sec. 2.2, "LLM
+Inference"): one new query token per sequence with ``h_q`` heads of size
+``d_h``; a KV cache of ``l`` tokens per sequence with ``h_kv`` heads of size
+``d_h``. The paper profiles decode with "random data with fixed lengths and a
+constant batch size" (Sec. 3.1); the five named workloads below stand in for
+that, with the shapes of the paper's models (Qwen3-class GQA, head size 128).
+
+Recipe (every choice that the paper leaves open):
+  * seed of workload ``i`` is ``1000 + i``; ``SeedSequence(seed).spawn(6)``
+    gives one independent stream each for [lengths, block table, q, k, v,
+    key-scale mask], so adding a tensor never shifts the others;
+  * q, K, V are N(0, 1) drawn as float32 (``standard_normal(dtype=float32)``)
+    in flat chunks of 2**20 elements, chunk c from a generator seeded by the
+    c-th child of that tensor's stream (so chunks can be drawn in parallel),
+    and, for bf16 workloads, rounded to nearest-even to bfloat16;
+  * "uniform in [a, b]" lengths are integers with both ends included;
+  * the paged pool holds exactly ``sum_b ceil(L_b / page)`` pages (plus
+    optional spares), handed out in the order of one random permutation;
+    unused block-table entries are -1;
+  * "5% of keys scaled x8" is a Bernoulli(0.05) draw per (pool token slot,
+    KV head) row of K only; the whole head_dim vector is scaled before the
+    bf16 cast (x8 is a power of two, so before/after the cast agree).
+"""
+
+from __future__ import annotations
+
+import dataclasses
+import math
+import os
+from concurrent.futures import ThreadPoolExecutor
+from typing import Optional, Sequence
+
+import numpy as np
+
+# Large tensors are drawn in chunks of this many elements, one child seed per
+# chunk (part of the recipe: changing it changes the drawn values).
+_DRAW_CHUNK = 1 << 20
+_THREADS = max(1, min(16, len(os.sched_getaffinity(0))))
+
+STREAMS = ("lengths", "block_table", "q", "k", "v", "key_mask")
+
+
+@dataclasses.dataclass(frozen=True)
+class WorkloadSpec:
+    """Shape and distribution of one decode-attention workload."""
+
+    name: str
+    batch: int
+    num_q_heads: int
+    num_kv_heads: int
+    head_dim: int
+    dtype: str  # "f32" or "bf16": dtype of q, K and V alike
+    lengths: tuple  # ("fixed", L) or ("uniform", lo, hi) or ("list", (L0, L1, ...))
+    max_ctx_len: int  # upper bound on every length (planning / block-table width)
+    layout: str = "contiguous"  # "contiguous" (packed ragged) or "paged"
+    page_size: int = 0
+    key_scale_frac: float = 0.0
+    key_scale: float = 8.0
+    seed: int = 0
+
+    @property
+    def group(self) -> int:
+        return self.num_q_heads // self.num_kv_heads
+
+    @property
+    def scale(self) -> np.float32:
+        """Softmax scale 1/sqrt(head_dim), as the float32 the kernels receive."""
+        return np.float32(1.0 / math.sqrt(self.head_dim))
+
+    @property
+    def elem_bytes(self) -> int:
+        return 4 if self.dtype == "f32" else 2
+
+    def replace(self, **kw) -> "WorkloadSpec":
+        return dataclasses.replace(self, **kw)
+
+
+# The five named workloads (sizes as stated for this build's targets).
+WORKLOADS = {
+    1: WorkloadSpec("tiny_f32_L2048", 1, 8, 2, 64, "f32", ("fixed", 2048), 2048, seed=1001),
+    2: WorkloadSpec("bf16_B1_L32768", 1, 32, 8, 128, "bf16", ("fixed", 32768), 32768, seed=1002),
+    3: WorkloadSpec("bf16_ragged_B16_L4k-64k", 16, 32, 8, 128, "bf16",
+                    ("uniform", 4096, 65536), 65536, seed=1003),
+    4: WorkloadSpec("bf16_paged16_B64_L2k-16k", 64, 32, 8, 128, "bf16",
+                    ("uniform", 2048, 16384), 16384, layout="paged", page_size=16,
+                    key_scale_frac=0.05, seed=1004),
+    5: WorkloadSpec("bf16_paged64_B8_L131072_G8", 8, 64, 8, 128, "bf16",
+                    ("fixed", 131072), 131072, layout="paged", page_size=64, seed=1005),
+}
+
+
+def f32_to_bf16_bits(x: np.ndarray) -> np.ndarray:
+    """Round float32 values to bfloat16 (nearest, ties to even); return the bit patterns."""
+    x = np.ascontiguousarray(x, dtype=np.float32)
+    u = x.view(np.uint32)
+    nan = np.isnan(x)
+    # Non-NaN patterns are below 0xFF800001, so adding at most 0x8000 cannot wrap.
+    r = ((np.where(nan, np.uint32(0), u) + np.uint32(0x7FFF) + ((u >> np.uint32(16)) & np.uint32(1)))
+         >> np.uint32(16)).astype(np.uint16)
+    if nan.any():
+        r[nan] = (u[nan] >> np.uint32(16)).astype(np.uint16) | np.uint16(0x0040)
+    return r
+
+
+def _draw_tensor(stream: np.random.SeedSequence, shape, dtype: str,
+                 row_scale: Optional[np.ndarray] = None) -> np.ndarray:
+    """N(0,1) tensor drawn in fixed chunks of _DRAW_CHUNK elements.
+
+    Chunk c is drawn from its own generator seeded by ``stream.spawn(n)[c]``, so
+    the values depend only on the seed and the shape, never on the thread count.
+    ``row_scale`` (optional) multiplies each row (all leading dims but the last)
+    before the bf16 cast.
+    """
+    n = int(np.prod(shape))
+    inner = shape[-1]
+    assert _DRAW_CHUNK % inner == 0
+    out = np.empty(n, dtype=np.float32 if dtype == "f32" else np.uint16)
+    nchunks = max(1, -(-n // _DRAW_CHUNK))
+    children = stream.spawn(nchunks)
+    rs = None if row_scale is None else row_scale.reshape(-1)
+
+    def work(c: int) -> None:
+        lo = c * _DRAW_CHUNK
+        hi = min(n, lo + _DRAW_CHUNK)
+        x = np.random.default_rng(children[c]).standard_normal(hi - lo, dtype=np.float32)
+        if rs is not None:
+            x = (x.reshape(-1, inner) * rs[lo // inner: hi // inner, None]).reshape(-1)
+        out[lo:hi] = x if dtype == "f32" else f32_to_bf16_bits(x)
+
+    if nchunks == 1:
+        work(0)
+    else:
+        with ThreadPoolExecutor(max_workers=min(_THREADS, nchunks)) as ex:
+            list(ex.map(work, range(nchunks)))
+    return out.reshape(shape)
+
+
+@dataclasses.dataclass
+class Workload:
+    """Host arrays of one drawn workload (bf16 data held as uint16 bit patterns)."""
+
+    spec: WorkloadSpec
+    q: np.ndarray  # [B, Hq, D]
+    ctx_lens: np.ndarray  # int32 [B]
+    # contiguous layout
+    k: Optional[np.ndarray] = None  # [T, Hkv, D]
+    v: Optional[np.ndarray] = None
+    seq_start: Optional[np.ndarray] = None  # int64 [B]
+    # paged layout
+    k_pages: Optional[np.ndarray] = None  # [P, page, Hkv, D]
+    v_pages: Optional[np.ndarray] = None
+    block_table: Optional[np.ndarray] = None  # int32 [B, max_pages], -1 padded
+
+    @property
+    def kv_bytes(self) -> int:
+        """Algorithmic K+V bytes of one step: each K and V element of every context once."""
+        s = self.spec
+        return int(self.ctx_lens.astype(np.int64).sum()) * s.num_kv_heads * s.head_dim * 2 * s.elem_bytes
+
+
+def draw_lengths(spec: WorkloadSpec, rng: np.random.Generator) -> np.ndarray:
+    kind = spec.lengths[0]
+    if kind == "fixed":
+        lens = np.full(spec.batch, spec.lengths[1], dtype=np.int64)
+    elif kind == "uniform":
+        lens = rng.integers(spec.lengths[1], spec.lengths[2], size=spec.batch, endpoint=True)
+    elif kind == "list":
+        lens = np.asarray(spec.lengths[1], dtype=np.int64)
+        assert lens.shape == (spec.batch,)
+    else:
+        raise ValueError(f"unknown length kind {kind!r}")
+    assert lens.min(initial=0) >= 0 and lens.max(initial=0) <= spec.max_ctx_len
+    return lens.astype(np.int32)
+
+
+def generate(spec: WorkloadSpec, seed: Optional[int] = None, *, gap_rows: int = 0,
+             spare_pages: int = 0, poison: bool = False) -> Workload:
+    """Draw one workload.
+
+    gap_rows:    contiguous layout only; rows left between consecutive sequences.
+    spare_pages: paged layout only; pool pages that no sequence uses.
+    poison:      fill every K/V row that no context covers (gaps, slots past
+                 L_b in a last page, spare pages) with NaN, so that a kernel
+                 that reads outside the contexts produces NaN.
+    """
+    seed = spec.seed if seed is None else seed
+    seqs = dict(zip(STREAMS, np.random.SeedSequence(seed).spawn(len(STREAMS))))
+    rng = {name: np.random.default_rng(s) for name, s in seqs.items()}
+    B, Hq, Hkv, D = spec.batch, spec.num_q_heads, spec.num_kv_heads, spec.head_dim
+    assert Hq % Hkv == 0
+    lens = draw_lengths(spec, rng["lengths"])
+    q = _draw_tensor(seqs["q"], (B, Hq, D), spec.dtype)
+    nan_bits = np.float32("nan") if spec.dtype == "f32" else np.uint16(0x7FC0)
+
+    if spec.layout == "contiguous":
+        starts = np.zeros(B, dtype=np.int64)
+        pos = 0
+        for b in range(B):
+            starts[b] = pos
+            pos += int(lens[b]) + gap_rows
+        T = max(pos, 1)
+        rows = (T, Hkv)
+        mask = None
+        if spec.key_scale_frac > 0:
+            mask = np.where(rng["key_mask"].random(rows) < spec.key_scale_frac,
+                            np.float32(spec.key_scale), np.float32(1.0))
+        k = _draw_tensor(seqs["k"], (T, Hkv, D), spec.dtype, mask)
+        v = _draw_tensor(seqs["v"], (T, Hkv, D), spec.dtype)
+        if poison:
+            covered = np.zeros(T, dtype=bool)
+            for b in range(B):
+                covered[starts[b]: starts[b] + lens[b]] = True
+            k[~covered] = nan_bits
+            v[~covered] = nan_bits
+        return Workload(spec, q, lens, k=k, v=v, seq_start=starts)
+
+    if spec.layout != "paged":
+        raise ValueError(spec.layout)
+    ps = spec.page_size
+    assert ps > 0
+    pages_per_seq = [(int(L) + ps - 1) // ps for L in lens]
+    used = sum(pages_per_seq)
+    pool = used + spare_pages
+    perm = rng["block_table"].permutation(pool).astype(np.int32)
+    max_pages = (spec.max_ctx_len + ps - 1) // ps
+    bt = np.full((B, max(max_pages, 1)), -1, dtype=np.int32)
+    pos = 0
+    for b in range(B):
+        n = pages_per_seq[b]
+        bt[b, :n] = perm[pos: pos + n]
+        pos += n
+    P = max(pool, 1)
+    rows = (P, ps, Hkv)
+    mask = None
+    if spec.key_scale_frac > 0:
+        mask = np.where(rng["key_mask"].random(rows) < spec.key_scale_frac,
+                        np.float32(spec.key_scale), np.float32(1.0))
+    kp = _draw_tensor(seqs["k"], (P, ps, Hkv, D), spec.dtype, mask)
+    vp = _draw_tensor(seqs["v"], (P, ps, Hkv, D), spec.dtype)
+    if poison:
+        covered = np.zeros((P, ps), dtype=bool)
+        for b in range(B):
+            t = np.arange(int(lens[b]))
+            covered[bt[b, t // ps], t % ps] = True
+        kp[~covered] = nan_bits
+        vp[~covered] = nan_bits
+    return Workload(spec, q, lens, k_pages=kp, v_pages=vp, block_table=bt)
+
+
+def small_spec(base: WorkloadSpec, lengths: Sequence[int], *, max_ctx_len: Optional[int] = None,
+               seed: Optional[int] = None, **kw) -> WorkloadSpec:
+    """A workload with the head shapes, dtype and layout of ``base`` but given lengths."""
+    lens = tuple(int(x) for x in lengths)
+    mcl = max(lens) if max_ctx_len is None else max_ctx_len
+    return base.replace(batch=len(lens), lengths=("list", lens), max_ctx_len=max(mcl, 1),
+                        seed=base.seed if seed is None else seed, **kw)
