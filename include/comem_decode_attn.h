@@ -1,0 +1,162 @@
+/*
+ * comem_decode_attn.h -- single-token decode attention over a long KV cache
+ * on AMD Instinct MI355X (gfx950).
+ *
+ * The operation (paper Sec. 2.2, "LLM Inference"): after prefill, each
+ * sequence b holds a key cache and a value cache of L_b tokens, each token a
+ * [h_kv, d_h] block; at every decode step the new token's key and value are
+ * appended first (so L_b counts the new token) and the one new query token,
+ * [h_q, d_h], attends over the whole cache. The paper states that this step
+ * is bound by HBM bandwidth because every generated token re-reads the entire
+ * KV cache (Sec. 2.2; latency model of Sec. 3.3). Query head h reads KV head
+ * h / G with G = h_q / h_kv (grouped-query attention, consecutive grouping).
+ * For query head h of sequence b:
+ *
+ *     s_t   = scale * dot(q[b, h, :], K_b[t, h / G, :])       t = 0 .. L_b-1
+ *     out   = sum_t softmax(s)_t * V_b[t, h / G, :]
+ *     lse   = ln sum_t exp(s_t)
+ *
+ * L_b = 0 gives out = 0 and lse = -inf. The agent's full history and the
+ * memory model's compressed context (summary plus recent buffer, Sec. 3.2)
+ * are both just a shorter or longer cache, so one API serves both.
+ *
+ * Execution: the key axis of each (sequence, KV head) is split across
+ * workgroups (split-K / flash-decoding); each split produces a partial output
+ * and its log-sum-exp, and the last split of each (sequence, KV head) to
+ * finish merges them in a fixed order, so results are bitwise reproducible.
+ * Both compute calls enqueue work on the given HIP stream and return; they
+ * never allocate, synchronise, or read device memory from the host.
+ *
+ * Ownership: the caller owns every device buffer (q, K, V, block table,
+ * lengths, outputs, workspace). The plan is owned by the library from
+ * comem_decode_attn_init until comem_decode_attn_destroy.
+ *
+ * Errors: every argument is checked on the host before any HIP call; a bad
+ * argument returns its status and enqueues nothing. Launch failures return
+ * COMEM_ERR_HIP. The library never aborts, exits or throws across this ABI.
+ * Device-side contract (not checked): 0 <= ctx_lens[b] <= max_ctx_len,
+ * contexts lie inside the given buffers, and for the paged call
+ * 0 <= block_table[b][i] < num_pages for every i < ceil(ctx_lens[b] /
+ * page_size). Block-table entries past that are never read.
+ */
+#ifndef COMEM_DECODE_ATTN_H
+#define COMEM_DECODE_ATTN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  COMEM_OK = 0,
+  COMEM_ERR_NULL_POINTER = 1,        /* a required pointer is NULL */
+  COMEM_ERR_INVALID_SHAPE = 2,       /* sizes, strides or bounds inconsistent */
+  COMEM_ERR_UNSUPPORTED = 3,         /* dtype, head_dim, GQA group or variant not built */
+  COMEM_ERR_MISALIGNED = 4,          /* pointer or byte stride not 16-byte aligned */
+  COMEM_ERR_WORKSPACE_TOO_SMALL = 5, /* workspace_bytes below what the call needs */
+  COMEM_ERR_BAD_HANDLE = 6,          /* NULL or foreign plan */
+  COMEM_ERR_HIP = 7,                 /* HIP runtime error (device query or launch) */
+  COMEM_ERR_NO_DEVICE = 8            /* plan made with device = COMEM_NO_DEVICE */
+} comem_status;
+
+typedef enum {
+  COMEM_F32 = 0, /* q, K, V in IEEE float32 */
+  COMEM_BF16 = 1 /* q, K, V in bfloat16 */
+} comem_dtype;
+
+typedef enum {
+  COMEM_VARIANT_AUTO = 0, /* bf16 -> matrix-core kernel; f32 -> vector kernel */
+  COMEM_VARIANT_VALU = 1, /* vector-ALU kernel (f32 and bf16) */
+  COMEM_VARIANT_MFMA = 2  /* matrix-core kernel (bf16 only) */
+} comem_variant;
+
+/* Pass as `device` to comem_decode_attn_init to make a plan without touching
+ * the HIP runtime (a gfx950 with 256 compute units is assumed). Such a plan
+ * sizes workspaces and validates arguments; compute calls with it return
+ * COMEM_ERR_NO_DEVICE after validation. */
+#define COMEM_NO_DEVICE (-1)
+
+typedef struct {
+  int32_t num_q_heads;  /* h_q > 0 */
+  int32_t num_kv_heads; /* h_kv > 0, h_q % h_kv == 0, G = h_q / h_kv in {1,2,4,8,16} */
+  int32_t head_dim;     /* d_h in {64, 128} */
+  int32_t dtype;        /* comem_dtype of q, K and V */
+  float scale;          /* softmax scale, finite and > 0 (1/sqrt(d_h) is usual) */
+  int32_t max_batch;    /* largest batch any call will pass (> 0) */
+  int64_t max_ctx_len;  /* largest context any call will pass (> 0) */
+  int32_t chunk_tokens; /* tokens per split: 0 = planned per call; else a multiple of 32 */
+  int32_t variant;      /* comem_variant */
+} comem_decode_attn_config;
+
+typedef struct comem_decode_attn_plan comem_decode_attn_plan;
+
+/* Validate `cfg`, query `device` (a HIP device ordinal, or COMEM_NO_DEVICE)
+ * for its compute-unit count, and create a plan. *workspace_bytes_out gets
+ * the workspace size that every call within the plan's limits fits in.
+ * The caller allocates the workspace (device memory, 256-byte aligned) and
+ * must zero-fill it once before its first use; the library keeps the
+ * counters it holds at zero between calls. A workspace must not be used by
+ * two calls that can run at the same time. */
+comem_status comem_decode_attn_init(const comem_decode_attn_config* cfg, int device,
+                                    comem_decode_attn_plan** plan_out,
+                                    size_t* workspace_bytes_out);
+
+/* Free a plan (NULL is a no-op returning COMEM_OK). */
+comem_status comem_decode_attn_destroy(comem_decode_attn_plan* plan);
+
+/* Static, human-readable text for a status code. */
+const char* comem_status_string(comem_status status);
+
+/* Tokens per split and number of splits a call would use (for tests and
+ * reports): same planning as the compute calls. */
+comem_status comem_decode_attn_plan_splits(const comem_decode_attn_plan* plan, int32_t batch,
+                                           int64_t max_ctx_len, size_t workspace_bytes,
+                                           int32_t* chunk_tokens_out, int32_t* num_splits_out);
+
+/* Contiguous / ragged cache (paper Sec. 2.2: K_cache, V_cache of l tokens,
+ * each token an [h_kv, d_h] block).
+ *   q          [batch, h_q, d_h] dense, dtype of the plan, 16-byte aligned.
+ *   k, v       element (b, t, hk, d) at k[(seq_start[b] + t) * stride_token
+ *              + hk * stride_head + d]; d contiguous. 16-byte aligned; the
+ *              byte sizes of both strides must be multiples of 16.
+ *   seq_start  device int64 [batch]: first row of each sequence.
+ *   ctx_lens   device int32 [batch]: L_b, including the appended token.
+ *   batch      0 <= batch <= plan max_batch (0 enqueues nothing).
+ *   max_ctx_len host bound >= every ctx_lens[b], <= plan max_ctx_len.
+ *   out        device float32 [batch, h_q, d_h], 16-byte aligned.
+ *   lse        device float32 [batch, h_q] (natural log) or NULL.
+ *   workspace  device buffer of workspace_bytes (see init).
+ *   hip_stream hipStream_t to enqueue on (NULL = default stream). */
+comem_status comem_decode_attn(const comem_decode_attn_plan* plan, const void* q, const void* k,
+                               const void* v, int64_t stride_token, int64_t stride_head,
+                               const int64_t* seq_start, const int32_t* ctx_lens, int32_t batch,
+                               int64_t max_ctx_len, float* out, float* lse, void* workspace,
+                               size_t workspace_bytes, void* hip_stream);
+
+/* Paged cache driven by a block table (the paging scheme that the paper's
+ * serving engine uses, cited in Sec. 1 and configured in Sec. 4.2).
+ *   k_pages, v_pages element (b, t, hk, d) at
+ *              k_pages[block_table[b * max_pages_per_seq + t / page_size] * stride_page
+ *                      + (t % page_size) * stride_token + hk * stride_head + d].
+ *              16-byte aligned; the byte sizes of all three strides must be
+ *              multiples of 16.
+ *   page_size  a power of two, 1 .. 4096.
+ *   num_pages  number of pages in the pool (> 0 when batch > 0).
+ *   block_table device int32 [batch, max_pages_per_seq], with
+ *              max_pages_per_seq >= ceil(max_ctx_len / page_size).
+ *   Other arguments as in comem_decode_attn. */
+comem_status comem_decode_attn_paged(const comem_decode_attn_plan* plan, const void* q,
+                                     const void* k_pages, const void* v_pages, int64_t stride_page,
+                                     int64_t stride_token, int64_t stride_head, int32_t page_size,
+                                     int64_t num_pages, const int32_t* block_table,
+                                     int32_t max_pages_per_seq, const int32_t* ctx_lens,
+                                     int32_t batch, int64_t max_ctx_len, float* out, float* lse,
+                                     void* workspace, size_t workspace_bytes, void* hip_stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* COMEM_DECODE_ATTN_H */

@@ -1,0 +1,203 @@
+"""Python binding of libcomem_attn.so (ctypes): argument marshalling only.
+
+The functions named like the C entry points pass plain integers (device
+pointers, strides, sizes) straight through and raise ``ComemError`` on a
+non-OK status. ``DecodeAttention`` is a convenience wrapper that takes torch
+tensors, reads their pointers and strides, and owns a zero-filled workspace;
+torch is used only for device memory and the current stream. Every step of
+the computation runs in the HIP kernels of the library: when the library has
+not been built this module raises instead of computing anything else.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional, Tuple
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(PKG, "libcomem_attn.so")
+
+OK, ERR_NULL_POINTER, ERR_INVALID_SHAPE, ERR_UNSUPPORTED, ERR_MISALIGNED = 0, 1, 2, 3, 4
+ERR_WORKSPACE_TOO_SMALL, ERR_BAD_HANDLE, ERR_HIP, ERR_NO_DEVICE = 5, 6, 7, 8
+F32, BF16 = 0, 1
+VARIANT_AUTO, VARIANT_VALU, VARIANT_MFMA = 0, 1, 2
+NO_DEVICE = -1
+
+EXPORTED = (
+    "comem_decode_attn_init", "comem_decode_attn_destroy", "comem_status_string",
+    "comem_decode_attn_plan_splits", "comem_decode_attn", "comem_decode_attn_paged",
+)
+
+
+class Config(ctypes.Structure):
+    _fields_ = [
+        ("num_q_heads", ctypes.c_int32),
+        ("num_kv_heads", ctypes.c_int32),
+        ("head_dim", ctypes.c_int32),
+        ("dtype", ctypes.c_int32),
+        ("scale", ctypes.c_float),
+        ("max_batch", ctypes.c_int32),
+        ("max_ctx_len", ctypes.c_int64),
+        ("chunk_tokens", ctypes.c_int32),
+        ("variant", ctypes.c_int32),
+    ]
+
+
+class ComemError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        self.status = status
+        super().__init__(f"{where}: status {status} ({status_string(status)})")
+
+
+_lib = None
+
+
+def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
+    """Load the built library once; raise if it has not been built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise RuntimeError(f"{path} not found: build it with `python -m paper_2605_30842_amd.build`")
+    lib = ctypes.CDLL(path)
+    vp, i32, i64, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t
+    lib.comem_decode_attn_init.argtypes = [ctypes.POINTER(Config), ctypes.c_int, ctypes.POINTER(vp),
+                                           ctypes.POINTER(sz)]
+    lib.comem_decode_attn_init.restype = ctypes.c_int
+    lib.comem_decode_attn_destroy.argtypes = [vp]
+    lib.comem_decode_attn_destroy.restype = ctypes.c_int
+    lib.comem_status_string.argtypes = [ctypes.c_int]
+    lib.comem_status_string.restype = ctypes.c_char_p
+    lib.comem_decode_attn_plan_splits.argtypes = [vp, i32, i64, sz, ctypes.POINTER(i32), ctypes.POINTER(i32)]
+    lib.comem_decode_attn_plan_splits.restype = ctypes.c_int
+    lib.comem_decode_attn.argtypes = [vp, vp, vp, vp, i64, i64, vp, vp, i32, i64, vp, vp, vp, sz, vp]
+    lib.comem_decode_attn.restype = ctypes.c_int
+    lib.comem_decode_attn_paged.argtypes = [vp, vp, vp, vp, i64, i64, i64, i32, i64, vp, i32, vp, i32, i64,
+                                            vp, vp, vp, sz, vp]
+    lib.comem_decode_attn_paged.restype = ctypes.c_int
+    _lib = lib
+    return lib
+
+
+def status_string(status: int) -> str:
+    return load_library().comem_status_string(int(status)).decode()
+
+
+def _check(status: int, where: str) -> None:
+    if status != OK:
+        raise ComemError(status, where)
+
+
+# ------------------------------------------------------------ C entry points
+
+
+def comem_decode_attn_init(cfg: Config, device: int) -> Tuple[int, int]:
+    """Create a plan; returns (plan handle, workspace bytes)."""
+    plan = ctypes.c_void_p()
+    ws = ctypes.c_size_t()
+    _check(load_library().comem_decode_attn_init(ctypes.byref(cfg), int(device), ctypes.byref(plan),
+                                                 ctypes.byref(ws)), "comem_decode_attn_init")
+    return plan.value, ws.value
+
+
+def comem_decode_attn_destroy(plan: int) -> None:
+    _check(load_library().comem_decode_attn_destroy(plan), "comem_decode_attn_destroy")
+
+
+def comem_decode_attn_plan_splits(plan: int, batch: int, max_ctx_len: int, workspace_bytes: int) -> Tuple[int, int]:
+    chunk, splits = ctypes.c_int32(), ctypes.c_int32()
+    _check(load_library().comem_decode_attn_plan_splits(plan, batch, max_ctx_len, workspace_bytes,
+                                                        ctypes.byref(chunk), ctypes.byref(splits)),
+           "comem_decode_attn_plan_splits")
+    return chunk.value, splits.value
+
+
+def comem_decode_attn(plan, q, k, v, stride_token, stride_head, seq_start, ctx_lens, batch, max_ctx_len,
+                      out, lse, workspace, workspace_bytes, stream) -> None:
+    _check(load_library().comem_decode_attn(plan, q, k, v, stride_token, stride_head, seq_start, ctx_lens,
+                                            batch, max_ctx_len, out, lse, workspace, workspace_bytes, stream),
+           "comem_decode_attn")
+
+
+def comem_decode_attn_paged(plan, q, k_pages, v_pages, stride_page, stride_token, stride_head, page_size,
+                            num_pages, block_table, max_pages_per_seq, ctx_lens, batch, max_ctx_len, out, lse,
+                            workspace, workspace_bytes, stream) -> None:
+    _check(load_library().comem_decode_attn_paged(plan, q, k_pages, v_pages, stride_page, stride_token,
+                                                  stride_head, page_size, num_pages, block_table,
+                                                  max_pages_per_seq, ctx_lens, batch, max_ctx_len, out, lse,
+                                                  workspace, workspace_bytes, stream),
+           "comem_decode_attn_paged")
+
+
+# ------------------------------------------------------------ torch wrapper
+
+
+class DecodeAttention:
+    """A plan plus its workspace, called with torch device tensors.
+
+    q: [B, Hq, D]; contiguous k, v: [T, Hkv, D] (any strides with d
+    contiguous); paged k, v: [P, page_size, Hkv, D]. Outputs are float32
+    [B, Hq, D] and [B, Hq] (natural-log lse).
+    """
+
+    def __init__(self, num_q_heads: int, num_kv_heads: int, head_dim: int, dtype: str, scale: float,
+                 max_batch: int, max_ctx_len: int, chunk_tokens: int = 0, variant: str = "auto",
+                 device: int = 0):
+        import torch
+
+        self.cfg = Config(num_q_heads, num_kv_heads, head_dim, BF16 if dtype == "bf16" else F32, float(scale),
+                          max_batch, max_ctx_len, chunk_tokens,
+                          {"auto": VARIANT_AUTO, "valu": VARIANT_VALU, "mfma": VARIANT_MFMA}[variant])
+        self.device = device
+        self.plan, self.workspace_bytes = comem_decode_attn_init(self.cfg, device)
+        self.workspace = torch.zeros(max(self.workspace_bytes, 256), dtype=torch.uint8, device=f"cuda:{device}")
+
+    def close(self) -> None:
+        if self.plan:
+            comem_decode_attn_destroy(self.plan)
+            self.plan = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:  # noqa: BLE001 - interpreter shutdown
+            pass
+
+    def splits(self, batch: int, max_ctx_len: int) -> Tuple[int, int]:
+        return comem_decode_attn_plan_splits(self.plan, batch, max_ctx_len, self.workspace_bytes)
+
+    def _outputs(self, q, out, lse):
+        import torch
+
+        B, Hq, D = q.shape
+        if out is None:
+            out = torch.empty((B, Hq, D), dtype=torch.float32, device=q.device)
+        return out, lse
+
+    @staticmethod
+    def _stream(stream):
+        import torch
+
+        return (stream if stream is not None else torch.cuda.current_stream()).cuda_stream
+
+    def forward(self, q, k, v, seq_start, ctx_lens, max_ctx_len: int, out=None, lse=None, stream=None):
+        out, lse = self._outputs(q, out, lse)
+        assert k.stride() == v.stride() and k.stride(-1) == 1
+        comem_decode_attn(self.plan, q.data_ptr(), k.data_ptr(), v.data_ptr(), k.stride(0), k.stride(1),
+                          seq_start.data_ptr(), ctx_lens.data_ptr(), q.shape[0], int(max_ctx_len),
+                          out.data_ptr(), None if lse is None else lse.data_ptr(), self.workspace.data_ptr(),
+                          self.workspace_bytes, self._stream(stream))
+        return out, lse
+
+    def forward_paged(self, q, k_pages, v_pages, block_table, ctx_lens, max_ctx_len: int, out=None, lse=None,
+                      stream=None):
+        out, lse = self._outputs(q, out, lse)
+        assert k_pages.stride() == v_pages.stride() and k_pages.stride(-1) == 1
+        comem_decode_attn_paged(self.plan, q.data_ptr(), k_pages.data_ptr(), v_pages.data_ptr(),
+                                k_pages.stride(0), k_pages.stride(1), k_pages.stride(2), k_pages.shape[1],
+                                k_pages.shape[0], block_table.data_ptr(), block_table.shape[1],
+                                ctx_lens.data_ptr(), q.shape[0], int(max_ctx_len), out.data_ptr(),
+                                None if lse is None else lse.data_ptr(), self.workspace.data_ptr(),
+                                self.workspace_bytes, self._stream(stream))
+        return out, lse

@@ -1,0 +1,320 @@
+// Host side of the decode-attention C ABI: argument validation (always before
+// any HIP call), split planning, kernel selection and launch.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdint>
+#include <cstring>
+#include <new>
+
+#include "attn_common.h"
+#include "comem_decode_attn.h"
+
+namespace comem {
+using KernelFn = void (*)(AttnParams);
+KernelFn select_mfma_kernel(int head_dim, bool paged);
+KernelFn select_valu_kernel(bool bf16, int head_dim, int group, bool paged);
+}  // namespace comem
+
+namespace {
+
+constexpr uint64_t kPlanMagic = 0x434f4d454d444131ull;  // "COMEMDA1"
+constexpr int kAssumedCUs = 256;                        // gfx950 (MI355X) without a device query
+constexpr int64_t kTargetWgsPerCu = 2;                  // workgroups per compute unit for one full round
+constexpr int64_t kMinChunk = 256;                      // tokens per split, lower bound
+constexpr int64_t kMaxChunk = 2048;                     // tokens per split, upper bound (auto plan)
+constexpr int64_t kMaxContext = int64_t{1} << 30;
+constexpr int kGridYZLimit = 65535;
+
+size_t align256(size_t x) { return (x + 255) & ~size_t{255}; }
+int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) & (a - 1)) == 0; }
+
+}  // namespace
+
+struct comem_decode_attn_plan {
+  uint64_t magic;
+  comem_decode_attn_config cfg;
+  int device;
+  int num_cus;
+  size_t ticket_bytes;
+  size_t workspace_bytes;
+};
+
+namespace {
+
+int group_of(const comem_decode_attn_config& c) { return c.num_q_heads / c.num_kv_heads; }
+int elem_bytes(const comem_decode_attn_config& c) { return c.dtype == COMEM_F32 ? 4 : 2; }
+
+// Workspace bytes for `slots` (sequence, split) partial results: ticket
+// counters, then per-head lse values, then per-head partial outputs.
+size_t slots_workspace_bytes(const comem_decode_attn_plan& p, int64_t slots) {
+  const size_t rows = static_cast<size_t>(slots) * static_cast<size_t>(p.cfg.num_q_heads);
+  return p.ticket_bytes + align256(rows * 4) + rows * static_cast<size_t>(p.cfg.head_dim) * 4;
+}
+
+// Workspace bytes a call with `batch` sequences and `splits` splits needs.
+// A single split writes the output directly and touches no workspace.
+size_t call_workspace_bytes(const comem_decode_attn_plan& p, int64_t batch, int64_t splits) {
+  return splits <= 1 ? 0 : slots_workspace_bytes(p, batch * splits);
+}
+
+// Choose tokens per split and the split count for one call.
+comem_status plan_call(const comem_decode_attn_plan& p, int64_t batch, int64_t max_ctx,
+                       size_t ws_bytes, int64_t* chunk_out, int64_t* splits_out) {
+  const int64_t L = max_ctx > 0 ? max_ctx : 1;
+  int64_t chunk;
+  if (p.cfg.chunk_tokens > 0) {
+    chunk = p.cfg.chunk_tokens;
+    if (call_workspace_bytes(p, batch, ceil_div(L, chunk)) > ws_bytes) return COMEM_ERR_WORKSPACE_TOO_SMALL;
+  } else {
+    const int64_t target = kTargetWgsPerCu * p.num_cus;
+    const int64_t per = ceil_div(batch * p.cfg.num_kv_heads * L, target);
+    chunk = kMinChunk;
+    while (chunk < per && chunk < kMaxChunk) chunk *= 2;
+    if (chunk < kMinChunk) chunk = kMinChunk;
+    if (chunk > kMaxChunk) chunk = kMaxChunk;
+    while (call_workspace_bytes(p, batch, ceil_div(L, chunk)) > ws_bytes) {
+      if (chunk >= L) return COMEM_ERR_WORKSPACE_TOO_SMALL;
+      chunk *= 2;
+    }
+  }
+  *chunk_out = chunk;
+  *splits_out = ceil_div(L, chunk);
+  return COMEM_OK;
+}
+
+comem_status validate_config(const comem_decode_attn_config& c) {
+  if (c.num_q_heads <= 0 || c.num_kv_heads <= 0 || c.num_q_heads % c.num_kv_heads != 0)
+    return COMEM_ERR_INVALID_SHAPE;
+  if (c.num_kv_heads > kGridYZLimit) return COMEM_ERR_INVALID_SHAPE;
+  const int G = group_of(c);
+  if (G != 1 && G != 2 && G != 4 && G != 8 && G != 16) return COMEM_ERR_UNSUPPORTED;
+  if (c.head_dim != 64 && c.head_dim != 128) return COMEM_ERR_UNSUPPORTED;
+  if (c.dtype != COMEM_F32 && c.dtype != COMEM_BF16) return COMEM_ERR_UNSUPPORTED;
+  if (!std::isfinite(c.scale) || !(c.scale > 0.f)) return COMEM_ERR_INVALID_SHAPE;
+  if (c.max_batch <= 0 || c.max_batch > kGridYZLimit) return COMEM_ERR_INVALID_SHAPE;
+  if (c.max_ctx_len <= 0 || c.max_ctx_len > kMaxContext) return COMEM_ERR_INVALID_SHAPE;
+  if (c.chunk_tokens < 0 || c.chunk_tokens % 32 != 0 || c.chunk_tokens > kMaxContext)
+    return COMEM_ERR_INVALID_SHAPE;
+  if (c.variant != COMEM_VARIANT_AUTO && c.variant != COMEM_VARIANT_VALU && c.variant != COMEM_VARIANT_MFMA)
+    return COMEM_ERR_UNSUPPORTED;
+  if (c.variant == COMEM_VARIANT_MFMA && c.dtype != COMEM_BF16) return COMEM_ERR_UNSUPPORTED;
+  return COMEM_OK;
+}
+
+const comem_decode_attn_plan* checked(const comem_decode_attn_plan* p) {
+  return (p != nullptr && p->magic == kPlanMagic) ? p : nullptr;
+}
+
+// Checks shared by both compute calls.
+comem_status validate_common(const comem_decode_attn_plan& p, const void* q, const void* k, const void* v,
+                             int64_t stride_token, int64_t stride_head, const int32_t* ctx_lens,
+                             int32_t batch, int64_t max_ctx_len, const float* out, const float* lse,
+                             const void* workspace) {
+  if (batch < 0 || batch > p.cfg.max_batch) return COMEM_ERR_INVALID_SHAPE;
+  if (max_ctx_len < 0 || max_ctx_len > p.cfg.max_ctx_len) return COMEM_ERR_INVALID_SHAPE;
+  if (batch == 0) return COMEM_OK;
+  if (q == nullptr || k == nullptr || v == nullptr || ctx_lens == nullptr || out == nullptr)
+    return COMEM_ERR_NULL_POINTER;
+  if (stride_token <= 0 || stride_head < 0) return COMEM_ERR_INVALID_SHAPE;
+  if (p.cfg.num_kv_heads > 1 && stride_head == 0) return COMEM_ERR_INVALID_SHAPE;
+  const int64_t e = elem_bytes(p.cfg);
+  if ((stride_token * e) % 16 != 0 || (stride_head * e) % 16 != 0) return COMEM_ERR_MISALIGNED;
+  if (!aligned(q, 16) || !aligned(k, 16) || !aligned(v, 16) || !aligned(out, 16)) return COMEM_ERR_MISALIGNED;
+  if (lse != nullptr && !aligned(lse, 4)) return COMEM_ERR_MISALIGNED;
+  if (workspace != nullptr && !aligned(workspace, 256)) return COMEM_ERR_MISALIGNED;
+  return COMEM_OK;
+}
+
+comem_status launch(const comem_decode_attn_plan& p, bool paged, comem::AttnParams& a, int64_t batch,
+                    int64_t splits, void* stream) {
+  const bool bf16 = p.cfg.dtype == COMEM_BF16;
+  const bool use_mfma = p.cfg.variant == COMEM_VARIANT_MFMA || (p.cfg.variant == COMEM_VARIANT_AUTO && bf16);
+  comem::KernelFn fn = use_mfma ? comem::select_mfma_kernel(p.cfg.head_dim, paged)
+                                : comem::select_valu_kernel(bf16, p.cfg.head_dim, group_of(p.cfg), paged);
+  if (fn == nullptr) return COMEM_ERR_UNSUPPORTED;
+  dim3 grid(static_cast<unsigned>(splits), static_cast<unsigned>(p.cfg.num_kv_heads),
+            static_cast<unsigned>(batch));
+  dim3 block(comem::kThreads);
+  void* args[] = {&a};
+  const hipError_t err = hipLaunchKernel(reinterpret_cast<const void*>(fn), grid, block, args, 0,
+                                         static_cast<hipStream_t>(stream));
+  return err == hipSuccess ? COMEM_OK : COMEM_ERR_HIP;
+}
+
+void fill_common(const comem_decode_attn_plan& p, comem::AttnParams& a, const void* q, const void* k,
+                 const void* v, int64_t stride_token, int64_t stride_head, const int32_t* ctx_lens,
+                 float* out, float* lse, void* workspace, int64_t batch, int64_t chunk, int64_t splits) {
+  const int64_t e = elem_bytes(p.cfg);
+  std::memset(&a, 0, sizeof(a));
+  a.q = static_cast<const char*>(q);
+  a.k = static_cast<const char*>(k);
+  a.v = static_cast<const char*>(v);
+  a.out = out;
+  a.lse = lse;
+  a.ctx_lens = ctx_lens;
+  a.stride_token = stride_token * e;
+  a.stride_head = stride_head * e;
+  a.num_q_heads = p.cfg.num_q_heads;
+  a.num_kv_heads = p.cfg.num_kv_heads;
+  a.group = group_of(p.cfg);
+  a.chunk = static_cast<int32_t>(chunk);
+  a.num_splits = static_cast<int32_t>(splits);
+  a.scale_log2 = p.cfg.scale * 1.4426950408889634f;
+  if (splits > 1) {
+    char* ws = static_cast<char*>(workspace);
+    const size_t slots = static_cast<size_t>(batch) * static_cast<size_t>(splits) *
+                         static_cast<size_t>(p.cfg.num_q_heads);
+    a.tickets = reinterpret_cast<uint32_t*>(ws);
+    a.lse_part = reinterpret_cast<float*>(ws + p.ticket_bytes);
+    a.o_part = reinterpret_cast<float*>(ws + p.ticket_bytes + align256(slots * 4));
+  }
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* comem_status_string(comem_status s) {
+  switch (s) {
+    case COMEM_OK: return "ok";
+    case COMEM_ERR_NULL_POINTER: return "a required pointer is NULL";
+    case COMEM_ERR_INVALID_SHAPE: return "invalid shape, stride or bound";
+    case COMEM_ERR_UNSUPPORTED: return "unsupported dtype, head_dim, GQA group, variant or device";
+    case COMEM_ERR_MISALIGNED: return "pointer or byte stride not suitably aligned";
+    case COMEM_ERR_WORKSPACE_TOO_SMALL: return "workspace too small for this call";
+    case COMEM_ERR_BAD_HANDLE: return "NULL or invalid plan";
+    case COMEM_ERR_HIP: return "HIP runtime error";
+    case COMEM_ERR_NO_DEVICE: return "plan was made without a device";
+  }
+  return "unknown status";
+}
+
+comem_status comem_decode_attn_init(const comem_decode_attn_config* cfg, int device,
+                                    comem_decode_attn_plan** plan_out, size_t* workspace_bytes_out) {
+  if (cfg == nullptr || plan_out == nullptr || workspace_bytes_out == nullptr) return COMEM_ERR_NULL_POINTER;
+  *plan_out = nullptr;
+  *workspace_bytes_out = 0;
+  const comem_status st = validate_config(*cfg);
+  if (st != COMEM_OK) return st;
+  if (device < COMEM_NO_DEVICE) return COMEM_ERR_INVALID_SHAPE;
+  int num_cus = kAssumedCUs;
+  if (device != COMEM_NO_DEVICE) {
+    int count = 0;
+    if (hipGetDeviceCount(&count) != hipSuccess) return COMEM_ERR_HIP;
+    if (device >= count) return COMEM_ERR_INVALID_SHAPE;
+    hipDeviceProp_t prop;
+    if (hipGetDeviceProperties(&prop, device) != hipSuccess) return COMEM_ERR_HIP;
+    if (std::strncmp(prop.gcnArchName, "gfx950", 6) != 0) return COMEM_ERR_UNSUPPORTED;
+    num_cus = prop.multiProcessorCount;
+  }
+  auto* p = new (std::nothrow) comem_decode_attn_plan;
+  if (p == nullptr) return COMEM_ERR_HIP;
+  p->magic = kPlanMagic;
+  p->cfg = *cfg;
+  p->device = device;
+  p->num_cus = num_cus > 0 ? num_cus : kAssumedCUs;
+  p->ticket_bytes = align256(static_cast<size_t>(cfg->max_batch) * cfg->num_kv_heads * 4);
+  // Largest number of (sequence, split) slots any call within the limits plans.
+  const int64_t B = cfg->max_batch, L = cfg->max_ctx_len;
+  int64_t slots;
+  if (cfg->chunk_tokens > 0) {
+    slots = B * ceil_div(L, cfg->chunk_tokens);
+  } else {
+    const int64_t target = kTargetWgsPerCu * p->num_cus;
+    const int64_t a = ceil_div(target, cfg->num_kv_heads) + B;
+    const int64_t b = B * ceil_div(L, kMaxChunk);
+    slots = a > b ? a : b;
+    const int64_t c = B * ceil_div(L, kMinChunk);
+    if (c < slots) slots = c;
+  }
+  p->workspace_bytes = slots_workspace_bytes(*p, slots);
+  *plan_out = p;
+  *workspace_bytes_out = p->workspace_bytes;
+  return COMEM_OK;
+}
+
+comem_status comem_decode_attn_destroy(comem_decode_attn_plan* plan) {
+  if (plan == nullptr) return COMEM_OK;
+  if (plan->magic != kPlanMagic) return COMEM_ERR_BAD_HANDLE;
+  plan->magic = 0;
+  delete plan;
+  return COMEM_OK;
+}
+
+comem_status comem_decode_attn_plan_splits(const comem_decode_attn_plan* plan, int32_t batch,
+                                           int64_t max_ctx_len, size_t workspace_bytes,
+                                           int32_t* chunk_tokens_out, int32_t* num_splits_out) {
+  const comem_decode_attn_plan* p = checked(plan);
+  if (p == nullptr) return COMEM_ERR_BAD_HANDLE;
+  if (chunk_tokens_out == nullptr || num_splits_out == nullptr) return COMEM_ERR_NULL_POINTER;
+  if (batch < 0 || batch > p->cfg.max_batch) return COMEM_ERR_INVALID_SHAPE;
+  if (max_ctx_len < 0 || max_ctx_len > p->cfg.max_ctx_len) return COMEM_ERR_INVALID_SHAPE;
+  int64_t chunk = 0, splits = 0;
+  const comem_status st = plan_call(*p, batch, max_ctx_len, workspace_bytes, &chunk, &splits);
+  if (st != COMEM_OK) return st;
+  *chunk_tokens_out = static_cast<int32_t>(chunk);
+  *num_splits_out = static_cast<int32_t>(splits);
+  return COMEM_OK;
+}
+
+comem_status comem_decode_attn(const comem_decode_attn_plan* plan, const void* q, const void* k,
+                               const void* v, int64_t stride_token, int64_t stride_head,
+                               const int64_t* seq_start, const int32_t* ctx_lens, int32_t batch,
+                               int64_t max_ctx_len, float* out, float* lse, void* workspace,
+                               size_t workspace_bytes, void* hip_stream) {
+  const comem_decode_attn_plan* p = checked(plan);
+  if (p == nullptr) return COMEM_ERR_BAD_HANDLE;
+  comem_status st = validate_common(*p, q, k, v, stride_token, stride_head, ctx_lens, batch, max_ctx_len,
+                                    out, lse, workspace);
+  if (st != COMEM_OK || batch == 0) return st;
+  if (seq_start == nullptr) return COMEM_ERR_NULL_POINTER;
+  if (!aligned(seq_start, 8)) return COMEM_ERR_MISALIGNED;
+  int64_t chunk = 0, splits = 0;
+  st = plan_call(*p, batch, max_ctx_len, workspace == nullptr ? 0 : workspace_bytes, &chunk, &splits);
+  if (st != COMEM_OK) return st;
+  if (p->device == COMEM_NO_DEVICE) return COMEM_ERR_NO_DEVICE;
+  comem::AttnParams a;
+  fill_common(*p, a, q, k, v, stride_token, stride_head, ctx_lens, out, lse, workspace, batch, chunk, splits);
+  a.seq_start = seq_start;
+  return launch(*p, false, a, batch, splits, hip_stream);
+}
+
+comem_status comem_decode_attn_paged(const comem_decode_attn_plan* plan, const void* q,
+                                     const void* k_pages, const void* v_pages, int64_t stride_page,
+                                     int64_t stride_token, int64_t stride_head, int32_t page_size,
+                                     int64_t num_pages, const int32_t* block_table,
+                                     int32_t max_pages_per_seq, const int32_t* ctx_lens,
+                                     int32_t batch, int64_t max_ctx_len, float* out, float* lse,
+                                     void* workspace, size_t workspace_bytes, void* hip_stream) {
+  const comem_decode_attn_plan* p = checked(plan);
+  if (p == nullptr) return COMEM_ERR_BAD_HANDLE;
+  comem_status st = validate_common(*p, q, k_pages, v_pages, stride_token, stride_head, ctx_lens, batch,
+                                    max_ctx_len, out, lse, workspace);
+  if (st != COMEM_OK || batch == 0) return st;
+  if (block_table == nullptr) return COMEM_ERR_NULL_POINTER;
+  if (page_size <= 0 || page_size > 4096 || (page_size & (page_size - 1)) != 0) return COMEM_ERR_INVALID_SHAPE;
+  if (num_pages <= 0 || stride_page <= 0) return COMEM_ERR_INVALID_SHAPE;
+  if (max_pages_per_seq <= 0 || max_pages_per_seq < ceil_div(max_ctx_len, page_size))
+    return COMEM_ERR_INVALID_SHAPE;
+  if ((stride_page * elem_bytes(p->cfg)) % 16 != 0) return COMEM_ERR_MISALIGNED;
+  if (!aligned(block_table, 4)) return COMEM_ERR_MISALIGNED;
+  int64_t chunk = 0, splits = 0;
+  st = plan_call(*p, batch, max_ctx_len, workspace == nullptr ? 0 : workspace_bytes, &chunk, &splits);
+  if (st != COMEM_OK) return st;
+  if (p->device == COMEM_NO_DEVICE) return COMEM_ERR_NO_DEVICE;
+  comem::AttnParams a;
+  fill_common(*p, a, q, k_pages, v_pages, stride_token, stride_head, ctx_lens, out, lse, workspace, batch,
+              chunk, splits);
+  a.block_table = block_table;
+  a.stride_page = stride_page * elem_bytes(p->cfg);
+  a.max_pages = max_pages_per_seq;
+  int shift = 0;
+  while ((1 << shift) < page_size) ++shift;
+  a.page_shift = shift;
+  a.page_mask = page_size - 1;
+  return launch(*p, true, a, batch, splits, hip_stream);
+}
+
+}  // extern "C"

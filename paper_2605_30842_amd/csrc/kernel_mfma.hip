@@ -1,0 +1,271 @@
+// Matrix-core (MFMA) decode-attention kernel for bf16 caches on gfx950.
+//
+// One workgroup = one (split j, KV head hk, sequence b); its 4 waves take
+// 32-token tiles of the split in turn. Per tile a wave computes
+//   S^T[token, head] = K_tile . Q^T    with v_mfma_f32_16x16x32_bf16
+// (16 tokens x 16 head columns per instruction; the G real heads of the GQA
+// group occupy the first G columns), runs the online softmax on the scores
+// in registers, and accumulates
+//   O[head, d] += P[head, token] . V_tile[token, d]
+// again with 16x16x32 MFMAs. P is split as P = P_hi + P_lo, both bf16, and
+// both halves are multiplied (two MFMAs), so the weights keep about 16
+// significant bits instead of bf16's 8.
+//
+// Operand layouts (lane = 16 * g + c, c in 0..15, g in 0..3):
+//   MFMA 16x16x32 reads, for A, row c and reduction elements 8g..8g+7 of the
+//   lane; for B, column c and the same reduction elements; it returns
+//   D[4g + r][c] in accumulator register r.
+//   QK:  A = K rows (token c of the sub-tile), reduction = head_dim slice
+//        32kb + 8g .. +8 -> one 16-byte load per (sub-tile, kb).
+//        B = Q rows (head c), same slice. Result: lane holds the score of
+//        head c for tokens 4g + r of each 16-token sub-tile.
+//   PV:  A = P: lane already holds head c's weights for the 8 tokens
+//        {16s + 4g + r}; they become reduction elements e = 4s + r.
+//        B = V: the same 8 tokens, column c standing for d = NT*c + n in
+//        n-tile n (NT = D/16). Loading V row (16s + 4g + r), bytes
+//        [2*NT*c, 2*NT*(c+1)) gives every n-tile's element at once, and
+//        those loads read whole 256-byte rows with 16 consecutive lanes.
+//        A v_perm per element pair regroups them into MFMA operands.
+// The reduction index of an MFMA is a dummy index, so any consistent
+// assignment of (lane, element) to tokens or head_dim positions is valid as
+// long as A and B use the same one, which they do by construction above.
+#include "attn_common.h"
+
+namespace comem {
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+
+template <int D>
+struct VRow;  // per-lane slice of one V row: NT bf16 values
+template <>
+struct VRow<128> {
+  u32x4 w;
+  __device__ uint32_t word(int i) const { return w[i]; }
+};
+template <>
+struct VRow<64> {
+  u32x2 w;
+  __device__ uint32_t word(int i) const { return w[i]; }
+};
+
+template <int D>
+struct Tile {
+  static constexpr int KB = D / 32;
+  u32x4 k[2][KB];   // [sub-tile][k-block]
+  VRow<D> v[2][4];  // [sub-tile][r]
+};
+
+__device__ inline bf16x8 as_bf16x8(u32x4 x) { return __builtin_bit_cast(bf16x8, x); }
+
+template <int D, bool PAGED>
+struct MfmaCtx {
+  const AttnParams& p;
+  const char* kb;  // K base for this (hk)
+  const char* vb;
+  int b;
+  int64_t seq0;
+  int t_end;
+  int c, g;
+  int64_t k_lane;     // c * stride_token
+  int64_t v_lane[4];  // (4g + r) * stride_token
+
+  __device__ void load(Tile<D>& T, int t0) const {
+    constexpr int KB = D / 32;
+    constexpr int VBYTES = D / 8;  // bytes of one lane's V slice (NT bf16)
+    const bool full = (t0 + 32 <= t_end) && (!PAGED || p.page_shift >= 4);
+    if (full) {
+#pragma unroll
+      for (int s = 0; s < 2; ++s) {
+        const int64_t base = uniform_i64(row_offset<PAGED>(p, b, seq0, t0 + 16 * s));
+        const char* kr = kb + base + k_lane + 16 * g;
+#pragma unroll
+        for (int kk = 0; kk < KB; ++kk) T.k[s][kk] = *reinterpret_cast<const u32x4*>(kr + 64 * kk);
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const char* vr = vb + base + v_lane[r] + VBYTES * c;
+          T.v[s][r].w = *reinterpret_cast<const decltype(T.v[s][r].w)*>(vr);
+        }
+      }
+    } else {
+      // Partial tile (or pages shorter than a sub-tile): per-lane rows, with
+      // tokens past the end clamped to the last valid row (their weight is 0).
+#pragma unroll
+      for (int s = 0; s < 2; ++s) {
+        const int tk = min(t0 + 16 * s + c, t_end - 1);
+        const char* kr = kb + row_offset<PAGED>(p, b, seq0, tk) + 16 * g;
+#pragma unroll
+        for (int kk = 0; kk < KB; ++kk) T.k[s][kk] = *reinterpret_cast<const u32x4*>(kr + 64 * kk);
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int tv = min(t0 + 16 * s + 4 * g + r, t_end - 1);
+          const char* vr = vb + row_offset<PAGED>(p, b, seq0, tv) + VBYTES * c;
+          T.v[s][r].w = *reinterpret_cast<const decltype(T.v[s][r].w)*>(vr);
+        }
+      }
+    }
+  }
+};
+
+template <int D>
+__device__ inline void compute_tile(const Tile<D>& T, int t0, int t_end, int c, int g,
+                                    const bf16x8 (&qop)[D / 32], float scale_log2, float& m_run,
+                                    float& l_run, f32x4 (&acc)[D / 16]) {
+  constexpr int KB = D / 32;
+  constexpr int NT = D / 16;
+  // Scores S^T: lane holds head c, tokens t0 + 16s + 4g + r.
+  f32x4 sc[2];
+#pragma unroll
+  for (int s = 0; s < 2; ++s) {
+    sc[s] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int kk = 0; kk < KB; ++kk)
+      sc[s] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(T.k[s][kk]), qop[kk], sc[s], 0, 0, 0);
+  }
+  float x[8];
+  float mt = -INFINITY;
+#pragma unroll
+  for (int s = 0; s < 2; ++s)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int t = t0 + 16 * s + 4 * g + r;
+      const float v = t < t_end ? sc[s][r] * scale_log2 : -INFINITY;
+      x[4 * s + r] = v;
+      mt = fmaxf(mt, v);
+    }
+  mt = fmaxf(mt, __shfl_xor(mt, 16));
+  mt = fmaxf(mt, __shfl_xor(mt, 32));
+  // Every tile holds at least one valid token, so m_new is finite.
+  const float m_new = fmaxf(m_run, mt);
+  const float alpha = fast_exp2(m_run - m_new);
+  if (__any(m_new > m_run)) {
+    float ar[4];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) ar[r] = __shfl(alpha, 4 * g + r);
+#pragma unroll
+    for (int n = 0; n < NT; ++n)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) acc[n][r] *= ar[r];
+  }
+  m_run = m_new;
+  float psum = 0.f;
+  uint32_t ph[4], pl[4];
+#pragma unroll
+  for (int e = 0; e < 8; e += 2) {
+    const float p0 = fast_exp2(x[e] - m_new);
+    const float p1 = fast_exp2(x[e + 1] - m_new);
+    psum += p0 + p1;
+    const uint32_t b0 = __float_as_uint(p0), b1 = __float_as_uint(p1);
+    ph[e / 2] = __builtin_amdgcn_perm(b1, b0, 0x07060302u);  // upper halves: truncated bf16
+    // remainders p - hi are exact in fp32; round them to nearest-even bf16
+    uint32_t r0 = __float_as_uint(p0 - __uint_as_float(b0 & 0xffff0000u));
+    uint32_t r1 = __float_as_uint(p1 - __uint_as_float(b1 & 0xffff0000u));
+    r0 += 0x7fffu + ((r0 >> 16) & 1u);
+    r1 += 0x7fffu + ((r1 >> 16) & 1u);
+    pl[e / 2] = __builtin_amdgcn_perm(r1, r0, 0x07060302u);
+  }
+  l_run = l_run * alpha + psum;
+  const bf16x8 pa_hi = as_bf16x8(u32x4{ph[0], ph[1], ph[2], ph[3]});
+  const bf16x8 pa_lo = as_bf16x8(u32x4{pl[0], pl[1], pl[2], pl[3]});
+#pragma unroll
+  for (int n = 0; n < NT; ++n) {
+    const uint32_t sel = (n & 1) ? 0x07060302u : 0x05040100u;
+    const int wi = n >> 1;
+    u32x4 vb;
+    vb[0] = __builtin_amdgcn_perm(T.v[0][1].word(wi), T.v[0][0].word(wi), sel);
+    vb[1] = __builtin_amdgcn_perm(T.v[0][3].word(wi), T.v[0][2].word(wi), sel);
+    vb[2] = __builtin_amdgcn_perm(T.v[1][1].word(wi), T.v[1][0].word(wi), sel);
+    vb[3] = __builtin_amdgcn_perm(T.v[1][3].word(wi), T.v[1][2].word(wi), sel);
+    acc[n] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(pa_hi, as_bf16x8(vb), acc[n], 0, 0, 0);
+    acc[n] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(pa_lo, as_bf16x8(vb), acc[n], 0, 0, 0);
+  }
+}
+
+template <int D, bool PAGED>
+__global__ __launch_bounds__(kThreads, 2) void decode_mfma_kernel(const AttnParams p) {
+  constexpr int KB = D / 32;
+  constexpr int NT = D / 16;
+  const int j = blockIdx.x, hk = blockIdx.y, b = blockIdx.z;
+  const int L = p.ctx_lens[b];
+  const int nsplit_b = L > 0 ? 1 + (L - 1) / p.chunk : 1;
+  if (j >= nsplit_b) return;
+  const int t_begin = j * p.chunk;
+  const int t_end = t_begin + min(L - t_begin, p.chunk);
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int c = lane & 15, g = lane >> 4;
+  const int G = p.group;
+
+  __shared__ WaveState<D> ws;
+
+  // Q operand: head c of the group (zero columns past G), slice 32kb + 8g.
+  bf16x8 qop[KB];
+  {
+    const char* qrow = p.q + (static_cast<int64_t>(b) * p.num_q_heads + hk * G + c) * D * 2;
+#pragma unroll
+    for (int kk = 0; kk < KB; ++kk) {
+      u32x4 qv = u32x4{0u, 0u, 0u, 0u};
+      if (c < G) qv = *reinterpret_cast<const u32x4*>(qrow + 64 * kk + 16 * g);
+      qop[kk] = as_bf16x8(qv);
+    }
+  }
+
+  MfmaCtx<D, PAGED> ctx{p, p.k + hk * p.stride_head, p.v + hk * p.stride_head, b,
+                        PAGED ? 0 : p.seq_start[b], t_end, c, g, c * p.stride_token, {}};
+#pragma unroll
+  for (int r = 0; r < 4; ++r) ctx.v_lane[r] = (4 * g + r) * p.stride_token;
+
+  float m_run = -INFINITY, l_run = 0.f;
+  f32x4 acc[NT];
+#pragma unroll
+  for (int n = 0; n < NT; ++n) acc[n] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  const int ntiles = (t_end - t_begin + 31) / 32;
+  int ti = w;
+  if (ti < ntiles) {
+    Tile<D> A, B;
+    ctx.load(A, t_begin + 32 * ti);
+    while (true) {
+      if (ti + kWaves < ntiles) ctx.load(B, t_begin + 32 * (ti + kWaves));
+      compute_tile<D>(A, t_begin + 32 * ti, t_end, c, g, qop, p.scale_log2, m_run, l_run, acc);
+      ti += kWaves;
+      if (ti >= ntiles) break;
+      if (ti + kWaves < ntiles) ctx.load(A, t_begin + 32 * (ti + kWaves));
+      compute_tile<D>(B, t_begin + 32 * ti, t_end, c, g, qop, p.scale_log2, m_run, l_run, acc);
+      ti += kWaves;
+      if (ti >= ntiles) break;
+    }
+  }
+
+  // Wave totals: l over the four lane groups; state to LDS.
+  l_run += __shfl_xor(l_run, 16);
+  l_run += __shfl_xor(l_run, 32);
+  if (g == 0 && c < G) {
+    ws.m[w][c] = m_run;
+    ws.l[w][c] = l_run;
+  }
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    const int h = 4 * g + r;
+    if (h < G) {
+#pragma unroll
+      for (int n = 0; n < NT; ++n) ws.o[w][h][NT * c + n] = acc[n][r];
+    }
+  }
+  __syncthreads();
+  finalize_split<D>(p, ws, b, hk, j, nsplit_b);
+}
+
+}  // namespace
+
+using KernelFn = void (*)(AttnParams);
+
+KernelFn select_mfma_kernel(int head_dim, bool paged) {
+  if (head_dim == 128) return paged ? decode_mfma_kernel<128, true> : decode_mfma_kernel<128, false>;
+  if (head_dim == 64) return paged ? decode_mfma_kernel<64, true> : decode_mfma_kernel<64, false>;
+  return nullptr;
+}
+
+}  // namespace comem

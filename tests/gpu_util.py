@@ -1,0 +1,96 @@
+"""Helpers shared by the GPU tests: move a drawn workload to the device, run
+the HIP path through the C ABI, and compare with the oracle."""
+
+from __future__ import annotations
+
+import sys
+
+import numpy as np
+
+TOL_BF16_ABS, TOL_BF16_REL = 2e-3, 1e-2  # official gate for bf16 inputs with fp32 accumulation
+TOL_F32_ABS = 1e-5                        # official gate for fp32 inputs
+TOL_DIAG = 1e-4                           # internal gate: |err| <= 1e-4 * max(1, max|ref|)
+
+
+def say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+def to_torch(arr, dtype, device):
+    import torch
+
+    if dtype == "bf16" and arr.dtype == np.uint16:
+        return torch.from_numpy(np.ascontiguousarray(arr).view(np.int16)).view(torch.bfloat16).to(device)
+    return torch.from_numpy(np.ascontiguousarray(arr)).to(device)
+
+
+class DeviceWorkload:
+    """Device copies of a drawn workload's arrays."""
+
+    def __init__(self, w, device="cuda:0"):
+        import torch
+
+        s = w.spec
+        self.w = w
+        self.spec = s
+        self.q = to_torch(w.q, s.dtype, device)
+        self.ctx_lens = torch.from_numpy(w.ctx_lens.astype(np.int32)).to(device)
+        if s.layout == "paged":
+            self.k = to_torch(w.k_pages, s.dtype, device)
+            self.v = to_torch(w.v_pages, s.dtype, device)
+            self.block_table = torch.from_numpy(w.block_table.astype(np.int32)).to(device)
+        else:
+            self.k = to_torch(w.k, s.dtype, device)
+            self.v = to_torch(w.v, s.dtype, device)
+            self.seq_start = torch.from_numpy(w.seq_start.astype(np.int64)).to(device)
+
+
+def make_op(spec, chunk=0, variant="auto", max_batch=None, max_ctx_len=None):
+    from paper_2605_30842_amd.binding import DecodeAttention
+
+    return DecodeAttention(spec.num_q_heads, spec.num_kv_heads, spec.head_dim, spec.dtype, float(spec.scale),
+                           max_batch or spec.batch, max_ctx_len or spec.max_ctx_len, chunk_tokens=chunk,
+                           variant=variant)
+
+
+def run(dw: DeviceWorkload, op, want_lse=True, max_ctx_len=None):
+    """One call of the HIP path; returns (out, lse) as numpy float32 (lse None if not asked)."""
+    import torch
+
+    s = dw.spec
+    B = s.batch
+    lse = torch.empty((B, s.num_q_heads), dtype=torch.float32, device=dw.q.device) if want_lse else None
+    mcl = s.max_ctx_len if max_ctx_len is None else max_ctx_len
+    if s.layout == "paged":
+        out, lse = op.forward_paged(dw.q, dw.k, dw.v, dw.block_table, dw.ctx_lens, mcl, lse=lse)
+    else:
+        out, lse = op.forward(dw.q, dw.k, dw.v, dw.seq_start, dw.ctx_lens, mcl, lse=lse)
+    torch.cuda.synchronize()
+    return out.cpu().numpy(), (None if lse is None else lse.cpu().numpy())
+
+
+def check(out, lse, ref_out, ref_lse, dtype, what=""):
+    """Assert the official gate (and, for bf16, the internal diagnostic gate); return max |err|."""
+    out = np.asarray(out, dtype=np.float64)
+    ref_out = np.asarray(ref_out, dtype=np.float64)
+    assert out.shape == ref_out.shape, what
+    assert np.all(np.isfinite(out)), f"{what}: non-finite output"
+    err = np.abs(out - ref_out)
+    scale = max(1.0, float(np.abs(ref_out).max(initial=0.0)))
+    if dtype == "f32":
+        assert err.max(initial=0) <= TOL_F32_ABS, f"{what}: max |err| {err.max():.3e}"
+    else:
+        bad = err > TOL_BF16_ABS + TOL_BF16_REL * np.abs(ref_out)
+        assert not bad.any(), f"{what}: {bad.sum()} elements outside 2e-3 + 1e-2|ref| (max {err.max():.3e})"
+        assert err.max(initial=0) <= TOL_DIAG * scale, f"{what}: diagnostic max |err| {err.max():.3e}"
+    if lse is not None and ref_lse is not None:
+        lse = np.asarray(lse, dtype=np.float64)
+        ref_lse = np.asarray(ref_lse, dtype=np.float64)
+        inf = np.isinf(ref_lse)
+        assert np.array_equal(np.isinf(lse), inf), f"{what}: lse -inf pattern"
+        assert np.all(lse[inf] == ref_lse[inf])
+        lerr = np.abs(lse[~inf] - ref_lse[~inf])
+        lim = (TOL_F32_ABS if dtype == "f32" else TOL_DIAG) * np.maximum(1.0, np.abs(ref_lse[~inf]))
+        assert np.all(lerr <= lim), f"{what}: lse max err {lerr.max(initial=0):.3e}"
+    return float(err.max(initial=0.0))

@@ -1,0 +1,207 @@
+"""C-ABI checks that need no GPU: exported symbols and host-side validation.
+
+Every call here uses a plan made with COMEM_NO_DEVICE, so nothing reaches the
+HIP runtime: argument errors come back before any HIP call, and a call whose
+arguments are all valid stops with COMEM_ERR_NO_DEVICE.
+"""
+
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2605_30842_amd import binding as B
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "comem_decode_attn.h")
+
+A = 1 << 20  # a 256-byte aligned fake device address (never dereferenced)
+
+
+def _declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(comem_[a-z_]+)\s*\(", text)))
+
+
+def test_header_declares_what_the_binding_expects():
+    assert _declared_functions() == sorted(B.EXPORTED)
+
+
+def test_library_exports_every_declared_symbol():
+    lib = B.load_library()
+    for name in _declared_functions():
+        assert hasattr(lib, name), name
+
+
+def _cfg(**kw):
+    base = dict(num_q_heads=32, num_kv_heads=8, head_dim=128, dtype=B.BF16, scale=0.088, max_batch=4,
+                max_ctx_len=4096, chunk_tokens=0, variant=B.VARIANT_AUTO)
+    base.update(kw)
+    return B.Config(**base)
+
+
+def _status_init(cfg, device=B.NO_DEVICE):
+    plan = ctypes.c_void_p()
+    ws = ctypes.c_size_t()
+    st = B.load_library().comem_decode_attn_init(ctypes.byref(cfg), device, ctypes.byref(plan), ctypes.byref(ws))
+    if st == B.OK:
+        B.comem_decode_attn_destroy(plan.value)
+    return st
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(num_q_heads=0), B.ERR_INVALID_SHAPE),
+    (dict(num_kv_heads=0), B.ERR_INVALID_SHAPE),
+    (dict(num_q_heads=30), B.ERR_INVALID_SHAPE),
+    (dict(num_q_heads=24, num_kv_heads=8), B.ERR_UNSUPPORTED),  # G = 3
+    (dict(num_q_heads=256, num_kv_heads=8), B.ERR_UNSUPPORTED),  # G = 32
+    (dict(head_dim=96), B.ERR_UNSUPPORTED),
+    (dict(dtype=7), B.ERR_UNSUPPORTED),
+    (dict(scale=0.0), B.ERR_INVALID_SHAPE),
+    (dict(scale=float("nan")), B.ERR_INVALID_SHAPE),
+    (dict(max_batch=0), B.ERR_INVALID_SHAPE),
+    (dict(max_batch=70000), B.ERR_INVALID_SHAPE),
+    (dict(max_ctx_len=0), B.ERR_INVALID_SHAPE),
+    (dict(max_ctx_len=(1 << 30) + 1), B.ERR_INVALID_SHAPE),
+    (dict(chunk_tokens=48), B.ERR_INVALID_SHAPE),
+    (dict(chunk_tokens=-32), B.ERR_INVALID_SHAPE),
+    (dict(variant=9), B.ERR_UNSUPPORTED),
+    (dict(variant=B.VARIANT_MFMA, dtype=B.F32), B.ERR_UNSUPPORTED),
+    (dict(), B.OK),
+    (dict(dtype=B.F32, head_dim=64, num_q_heads=8, num_kv_heads=2), B.OK),
+])
+def test_init_validation(kw, status):
+    assert _status_init(_cfg(**kw)) == status
+
+
+def test_init_null_arguments():
+    lib = B.load_library()
+    plan = ctypes.c_void_p()
+    ws = ctypes.c_size_t()
+    assert lib.comem_decode_attn_init(None, -1, ctypes.byref(plan), ctypes.byref(ws)) == B.ERR_NULL_POINTER
+    cfg = _cfg()
+    assert lib.comem_decode_attn_init(ctypes.byref(cfg), -1, None, ctypes.byref(ws)) == B.ERR_NULL_POINTER
+    assert lib.comem_decode_attn_init(ctypes.byref(cfg), -2, ctypes.byref(plan), ctypes.byref(ws)) == \
+        B.ERR_INVALID_SHAPE
+
+
+def test_status_strings_and_null_destroy():
+    for s in range(9):
+        assert B.status_string(s) and B.status_string(s) != "unknown status"
+    assert B.status_string(99) == "unknown status"
+    assert B.load_library().comem_decode_attn_destroy(None) == B.OK
+
+
+@pytest.fixture
+def plan():
+    p, ws = B.comem_decode_attn_init(_cfg(), B.NO_DEVICE)
+    yield p, ws
+    B.comem_decode_attn_destroy(p)
+
+
+def _contig_args(plan, ws, **kw):
+    args = dict(plan=plan, q=A, k=A, v=A, stride_token=8 * 128, stride_head=128, seq_start=A, ctx_lens=A,
+                batch=2, max_ctx_len=4096, out=A, lse=A, workspace=A, workspace_bytes=ws, stream=None)
+    args.update(kw)
+    return args
+
+
+def _call(args):
+    lib = B.load_library()
+    return lib.comem_decode_attn(*args.values())
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(), B.ERR_NO_DEVICE),
+    (dict(batch=0, q=None), B.OK),
+    (dict(batch=-1), B.ERR_INVALID_SHAPE),
+    (dict(batch=5), B.ERR_INVALID_SHAPE),
+    (dict(max_ctx_len=4097), B.ERR_INVALID_SHAPE),
+    (dict(max_ctx_len=-1), B.ERR_INVALID_SHAPE),
+    (dict(q=None), B.ERR_NULL_POINTER),
+    (dict(k=None), B.ERR_NULL_POINTER),
+    (dict(v=None), B.ERR_NULL_POINTER),
+    (dict(ctx_lens=None), B.ERR_NULL_POINTER),
+    (dict(out=None), B.ERR_NULL_POINTER),
+    (dict(seq_start=None), B.ERR_NULL_POINTER),
+    (dict(lse=None), B.ERR_NO_DEVICE),
+    (dict(stride_token=0), B.ERR_INVALID_SHAPE),
+    (dict(stride_head=0), B.ERR_INVALID_SHAPE),
+    (dict(stride_token=8 * 128 + 4), B.ERR_MISALIGNED),
+    (dict(stride_head=132), B.ERR_MISALIGNED),
+    (dict(q=A + 8), B.ERR_MISALIGNED),
+    (dict(k=A + 2), B.ERR_MISALIGNED),
+    (dict(v=A + 4), B.ERR_MISALIGNED),
+    (dict(out=A + 4), B.ERR_MISALIGNED),
+    (dict(lse=A + 2), B.ERR_MISALIGNED),
+    (dict(workspace=A + 16), B.ERR_MISALIGNED),
+    (dict(seq_start=A + 4), B.ERR_MISALIGNED),
+    (dict(workspace_bytes=64), B.ERR_NO_DEVICE),  # planner falls back to fewer, longer splits
+    (dict(workspace=None, workspace_bytes=0), B.ERR_NO_DEVICE),
+])
+def test_contiguous_validation(plan, kw, status):
+    p, ws = plan
+    assert _call(_contig_args(p, ws, **kw)) == status
+
+
+def test_bad_handle():
+    args = _contig_args(None, 0)
+    assert _call(args) == B.ERR_BAD_HANDLE
+    junk = ctypes.create_string_buffer(256)
+    args = _contig_args(ctypes.addressof(junk), 0)
+    assert _call(args) == B.ERR_BAD_HANDLE
+
+
+def _paged_args(plan, ws, **kw):
+    args = dict(plan=plan, q=A, k=A, v=A, stride_page=16 * 8 * 128, stride_token=8 * 128, stride_head=128,
+                page_size=16, num_pages=100, block_table=A, max_pages=256, ctx_lens=A, batch=2,
+                max_ctx_len=4096, out=A, lse=A, workspace=A, workspace_bytes=ws, stream=None)
+    args.update(kw)
+    return args
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(), B.ERR_NO_DEVICE),
+    (dict(block_table=None), B.ERR_NULL_POINTER),
+    (dict(page_size=0), B.ERR_INVALID_SHAPE),
+    (dict(page_size=24), B.ERR_INVALID_SHAPE),
+    (dict(page_size=8192), B.ERR_INVALID_SHAPE),
+    (dict(num_pages=0), B.ERR_INVALID_SHAPE),
+    (dict(stride_page=0), B.ERR_INVALID_SHAPE),
+    (dict(max_pages=255), B.ERR_INVALID_SHAPE),
+    (dict(stride_page=16 * 8 * 128 + 4), B.ERR_MISALIGNED),
+    (dict(block_table=A + 2), B.ERR_MISALIGNED),
+    (dict(page_size=1, max_pages=4096), B.ERR_NO_DEVICE),
+    (dict(batch=0, block_table=None), B.OK),
+])
+def test_paged_validation(plan, kw, status):
+    p, ws = plan
+    assert B.load_library().comem_decode_attn_paged(*_paged_args(p, ws, **kw).values()) == status
+
+
+def test_forced_chunk_needs_room():
+    p, ws = B.comem_decode_attn_init(_cfg(chunk_tokens=32), B.NO_DEVICE)
+    try:
+        assert B.comem_decode_attn_plan_splits(p, 4, 4096, ws) == (32, 128)
+        st = B.load_library().comem_decode_attn(*_contig_args(p, ws, batch=4, workspace_bytes=ws - 1).values())
+        assert st == B.ERR_WORKSPACE_TOO_SMALL
+    finally:
+        B.comem_decode_attn_destroy(p)
+
+
+@pytest.mark.parametrize("batch,L", [(1, 32768), (16, 65536), (64, 16384), (8, 131072), (1, 1), (3, 300)])
+def test_auto_plan_fits_init_workspace(batch, L):
+    """Every call within the plan's limits fits the workspace size init reports."""
+    cfg = _cfg(max_batch=max(batch, 1), max_ctx_len=L)
+    p, ws = B.comem_decode_attn_init(cfg, B.NO_DEVICE)
+    try:
+        for b in sorted({1, max(1, batch // 2), batch}):
+            for l in sorted(x for x in {1, 33, L // 3 + 1, L} if x <= L):
+                chunk, splits = B.comem_decode_attn_plan_splits(p, b, l, ws)
+                assert chunk % 32 == 0 and splits == -(-l // chunk)
+                chunk2, _ = B.comem_decode_attn_plan_splits(p, b, l, 1 << 40)
+                assert chunk2 == chunk, "init workspace forced a coarser plan"
+    finally:
+        B.comem_decode_attn_destroy(p)

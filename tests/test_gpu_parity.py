@@ -1,0 +1,223 @@
+"""HIP path vs the fp64 oracle, element by element, through the C ABI.
+
+Small cases span several 32-token tiles, several splits and ragged tails;
+edge cases cover empty and one-token contexts, every supported GQA group and
+head size, page sizes below and above a tile, NaN-poisoned memory outside the
+contexts, strided (fused) K/V buffers and bitwise reproducibility.
+"""
+
+import numpy as np
+import pytest
+
+import oracle.decode_attention as da
+from tests.gpu_util import DeviceWorkload, check, make_op, run, say
+from workloads.synth import WORKLOADS, generate, small_spec
+
+pytestmark = pytest.mark.gpu
+
+RAGGED = [1, 31, 32, 33, 100, 1000, 4097]
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _cuda():
+    import torch
+
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    from paper_2605_30842_amd import binding
+
+    binding.load_library()
+    yield
+
+
+def _case(spec, variant="auto", chunk=0, seed=None, **gen):
+    w = generate(spec, seed=seed, **gen)
+    say(f"case {spec.name} B={spec.batch} lens={w.ctx_lens.tolist()[:8]} G={spec.group} D={spec.head_dim} "
+        f"{spec.dtype} {spec.layout} ps={spec.page_size} variant={variant} chunk={chunk}")
+    dw = DeviceWorkload(w)
+    op = make_op(spec, chunk=chunk, variant=variant)
+    out, lse = run(dw, op)
+    ref_out, ref_lse = da.reference(w)
+    return w, dw, op, out, lse, ref_out, ref_lse
+
+
+def test_fp32_tiny_workload():
+    w, dw, op, out, lse, ro, rl = _case(WORKLOADS[1])
+    check(out, lse, ro, rl, "f32", "fp32 L=2048")
+
+
+@pytest.mark.parametrize("chunk", [0, 32, 64, 256])
+def test_fp32_ragged(chunk):
+    spec = small_spec(WORKLOADS[1], RAGGED, seed=21)
+    _, _, _, out, lse, ro, rl = _case(spec, chunk=chunk)
+    check(out, lse, ro, rl, "f32", f"fp32 ragged chunk={chunk}")
+
+
+@pytest.mark.parametrize("variant", ["mfma", "valu"])
+@pytest.mark.parametrize("chunk", [0, 32, 96, 256, 2048])
+def test_bf16_ragged_contiguous(variant, chunk):
+    spec = small_spec(WORKLOADS[2], RAGGED, seed=22)
+    _, _, _, out, lse, ro, rl = _case(spec, variant=variant, chunk=chunk)
+    check(out, lse, ro, rl, "bf16", f"bf16 ragged {variant} chunk={chunk}")
+
+
+@pytest.mark.parametrize("variant", ["mfma", "valu"])
+@pytest.mark.parametrize("G", [1, 2, 4, 8, 16])
+@pytest.mark.parametrize("D", [64, 128])
+def test_groups_and_head_dims(variant, G, D):
+    spec = small_spec(WORKLOADS[2], [5, 77, 700], seed=23 + G + D).replace(
+        num_q_heads=2 * G, num_kv_heads=2, head_dim=D)
+    _, _, _, out, lse, ro, rl = _case(spec, variant=variant, chunk=128)
+    check(out, lse, ro, rl, "bf16", f"G={G} D={D} {variant}")
+
+
+@pytest.mark.parametrize("G,D", [(4, 64), (8, 128), (16, 64)])
+def test_fp32_groups(G, D):
+    spec = small_spec(WORKLOADS[1], [3, 200], seed=24).replace(num_q_heads=2 * G, num_kv_heads=2, head_dim=D)
+    _, _, _, out, lse, ro, rl = _case(spec, chunk=64)
+    check(out, lse, ro, rl, "f32", f"fp32 G={G} D={D}")
+
+
+@pytest.mark.parametrize("variant", ["mfma", "valu"])
+@pytest.mark.parametrize("ps", [1, 8, 16, 64, 128])
+def test_paged_small(variant, ps):
+    spec = small_spec(WORKLOADS[4], RAGGED, seed=25 + ps, max_ctx_len=4224).replace(page_size=ps)
+    _, _, _, out, lse, ro, rl = _case(spec, variant=variant, chunk=256, spare_pages=3)
+    check(out, lse, ro, rl, "bf16", f"paged ps={ps} {variant}")
+
+
+@pytest.mark.parametrize("variant", ["mfma", "valu"])
+def test_empty_and_one_token(variant):
+    spec = small_spec(WORKLOADS[2], [0, 1, 0, 1, 2], seed=26)
+    w, _, _, out, lse, ro, rl = _case(spec, variant=variant)
+    for b in (0, 2):
+        assert np.array_equal(out[b], np.zeros_like(out[b])) and np.all(lse[b] == -np.inf)
+    for b in (1, 3):
+        v0 = da.widen(w.v[w.seq_start[b]], "bf16")  # [Hkv, D]
+        assert np.array_equal(out[b].astype(np.float64), np.repeat(v0, spec.group, axis=0)), "L=1 must be exact"
+    check(out, lse, ro, rl, "bf16", f"empty/one {variant}")
+
+
+@pytest.mark.parametrize("variant", ["mfma", "valu"])
+def test_zero_query_gives_mean_of_structured_values(variant):
+    """q = 0: every weight equal, out = mean of V. V[t] = (t mod 97) / 32 is exact in bf16."""
+    from workloads.synth import f32_to_bf16_bits
+
+    L = 5000
+    spec = small_spec(WORKLOADS[2], [L], seed=27)
+    w = generate(spec)
+    w.q[:] = 0
+    vals = ((np.arange(L) % 97) / 32.0).astype(np.float32)
+    w.v[:] = f32_to_bf16_bits(np.broadcast_to(vals[:, None, None], w.v.shape).copy())
+    say(f"case q=0 structured V {variant}")
+    op = make_op(spec, variant=variant, chunk=256)
+    out, lse = run(DeviceWorkload(w), op)
+    mean = float(np.sum(vals.astype(np.float64)) / L)
+    assert np.abs(out - mean).max() <= 2e-6 * mean, np.abs(out - mean).max()
+    assert np.abs(lse - np.log(L)).max() <= 1e-5
+
+
+@pytest.mark.parametrize("variant", ["mfma", "valu"])
+def test_nan_poison_outside_contexts(variant):
+    spec = small_spec(WORKLOADS[2], [5, 33, 0, 300], seed=28)
+    _, _, _, out, lse, ro, rl = _case(spec, variant=variant, chunk=64, gap_rows=40, poison=True)
+    check(out, lse, ro, rl, "bf16", f"poison contiguous {variant}")
+    spec = small_spec(WORKLOADS[4], [5, 33, 0, 300], seed=29, max_ctx_len=320).replace(page_size=16)
+    _, _, _, out, lse, ro, rl = _case(spec, variant=variant, chunk=64, spare_pages=4, poison=True)
+    check(out, lse, ro, rl, "bf16", f"poison paged {variant}")
+
+
+@pytest.mark.parametrize("variant", ["mfma", "valu"])
+@pytest.mark.parametrize("ps", [16, 64])
+def test_paged_equals_contiguous_bitwise(variant, ps):
+    """Same logical rows, same split plan: the paged and packed calls agree bit for bit."""
+    import torch
+
+    spec = small_spec(WORKLOADS[4], [17, 2048, 999, 64], seed=30, max_ctx_len=2048).replace(page_size=ps)
+    w = generate(spec, spare_pages=2)
+    say(f"case paged==contiguous ps={ps} {variant}")
+    dwp = DeviceWorkload(w)
+    op = make_op(spec, variant=variant, chunk=256)
+    out_p, lse_p = run(dwp, op)
+    lens = w.ctx_lens.astype(np.int64)
+    starts = np.concatenate([[0], np.cumsum(lens)[:-1]])
+    kp = da.paged_context  # logical gather on the host
+    k = np.concatenate([kp(w.k_pages, w.block_table, w.ctx_lens, b) for b in range(spec.batch)])
+    v = np.concatenate([kp(w.v_pages, w.block_table, w.ctx_lens, b) for b in range(spec.batch)])
+    wc = generate(spec.replace(layout="contiguous", page_size=0))
+    wc.q[:] = w.q
+    wc.k, wc.v, wc.seq_start, wc.ctx_lens = k, v, starts, w.ctx_lens
+    out_c, lse_c = run(DeviceWorkload(wc), op)
+    assert np.array_equal(out_p, out_c) and np.array_equal(lse_p, lse_c)
+    torch.cuda.synchronize()
+
+
+@pytest.mark.parametrize("variant", ["mfma", "valu"])
+def test_bitwise_reproducible(variant):
+    spec = small_spec(WORKLOADS[2], [4096, 3000, 77], seed=31)
+    w = generate(spec)
+    dw = DeviceWorkload(w)
+    op = make_op(spec, variant=variant, chunk=128)
+    say(f"case reproducible {variant}")
+    first = run(dw, op)
+    for _ in range(3):
+        again = run(dw, op)
+        assert np.array_equal(first[0], again[0]) and np.array_equal(first[1], again[1])
+
+
+@pytest.mark.parametrize("variant", ["mfma", "valu"])
+def test_fused_kv_buffer_strides(variant):
+    """K and V interleaved in one [T, 2, Hkv, D] buffer: stride_token = 2 * Hkv * D."""
+    import torch
+
+    spec = small_spec(WORKLOADS[2], [300, 1, 129], seed=32)
+    w = generate(spec)
+    dw = DeviceWorkload(w)
+    T = dw.k.shape[0]
+    fused = torch.empty((T, 2, spec.num_kv_heads, spec.head_dim), dtype=dw.k.dtype, device=dw.k.device)
+    fused[:, 0] = dw.k
+    fused[:, 1] = dw.v
+    dw.k, dw.v = fused[:, 0], fused[:, 1]
+    op = make_op(spec, variant=variant, chunk=64)
+    say(f"case fused kv {variant}")
+    out, lse = run(dw, op)
+    ro, rl = da.reference(w)
+    check(out, lse, ro, rl, "bf16", f"fused kv {variant}")
+
+
+def test_workspace_reused_across_changing_calls():
+    """Ticket counters return to zero: calls with different split counts share one workspace."""
+    base = small_spec(WORKLOADS[2], [2000], seed=33, max_ctx_len=8192)
+    op = make_op(base.replace(batch=3), chunk=64, max_batch=3, max_ctx_len=8192)
+    for i, lens in enumerate([[2000, 5, 8192], [64, 65, 63], [8192, 8192, 8192], [1, 0, 4000], [2000]]):
+        spec = small_spec(base, lens, seed=40 + i, max_ctx_len=8192)
+        w = generate(spec)
+        say(f"case workspace reuse call {i} lens={lens}")
+        out, lse = run(DeviceWorkload(w), op, max_ctx_len=max(lens))
+        ro, rl = da.reference(w)
+        check(out, lse, ro, rl, "bf16", f"reuse call {i}")
+
+
+def test_lse_optional():
+    spec = small_spec(WORKLOADS[2], [100, 3000], seed=34)
+    w = generate(spec)
+    say("case lse=None")
+    out, lse = run(DeviceWorkload(w), make_op(spec, chunk=256), want_lse=False)
+    assert lse is None
+    check(out, None, *da.reference(w), "bf16", "no lse")
+
+
+@pytest.mark.parametrize("variant", ["mfma", "valu"])
+def test_split_merge_stress(variant):
+    """Up to 256 splits per (sequence, KV head) and 16k workgroups: every split's
+    partial result must reach the merging workgroup, call after call."""
+    spec = small_spec(WORKLOADS[2], [8192, 4096, 8191, 33, 6000, 8192, 1, 7777], seed=35)
+    w = generate(spec)
+    dw = DeviceWorkload(w)
+    op = make_op(spec, variant=variant, chunk=32)
+    say(f"case split-merge stress {variant} splits={op.splits(spec.batch, spec.max_ctx_len)}")
+    ro, rl = da.reference(w)
+    first = run(dw, op)
+    check(*first, ro, rl, "bf16", f"stress {variant}")
+    for _ in range(4):
+        again = run(dw, op)
+        assert np.array_equal(first[0], again[0]) and np.array_equal(first[1], again[1])
