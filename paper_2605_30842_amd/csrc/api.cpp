@@ -12,7 +12,8 @@
 
 namespace comem {
 using KernelFn = void (*)(AttnParams);
-KernelFn select_mfma_kernel(int head_dim, bool paged);
+KernelFn select_mfma_kernel(int head_dim, bool paged, int page_size);
+int mfma_max_split_pages();
 KernelFn select_valu_kernel(bool bf16, int head_dim, int group, bool paged);
 }  // namespace comem
 
@@ -25,6 +26,7 @@ constexpr int64_t kMinChunk = 256;                      // tokens per split, low
 constexpr int64_t kMaxChunk = 2048;                     // tokens per split, upper bound (auto plan)
 constexpr int64_t kMaxContext = int64_t{1} << 30;
 constexpr int kGridYZLimit = 65535;
+constexpr int64_t kMaxTokenStrideBytes = int64_t{1} << 26;  // lane offsets within a tile stay 32-bit
 
 size_t align256(size_t x) { return (x + 255) & ~size_t{255}; }
 int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
@@ -121,18 +123,22 @@ comem_status validate_common(const comem_decode_attn_plan& p, const void* q, con
   if (p.cfg.num_kv_heads > 1 && stride_head == 0) return COMEM_ERR_INVALID_SHAPE;
   const int64_t e = elem_bytes(p.cfg);
   if ((stride_token * e) % 16 != 0 || (stride_head * e) % 16 != 0) return COMEM_ERR_MISALIGNED;
+  if (stride_token * e > kMaxTokenStrideBytes) return COMEM_ERR_INVALID_SHAPE;
   if (!aligned(q, 16) || !aligned(k, 16) || !aligned(v, 16) || !aligned(out, 16)) return COMEM_ERR_MISALIGNED;
   if (lse != nullptr && !aligned(lse, 4)) return COMEM_ERR_MISALIGNED;
   if (workspace != nullptr && !aligned(workspace, 256)) return COMEM_ERR_MISALIGNED;
   return COMEM_OK;
 }
 
+bool uses_mfma(const comem_decode_attn_plan& p) {
+  return p.cfg.variant == COMEM_VARIANT_MFMA || (p.cfg.variant == COMEM_VARIANT_AUTO && p.cfg.dtype == COMEM_BF16);
+}
+
 comem_status launch(const comem_decode_attn_plan& p, bool paged, comem::AttnParams& a, int64_t batch,
                     int64_t splits, void* stream) {
   const bool bf16 = p.cfg.dtype == COMEM_BF16;
-  const bool use_mfma = p.cfg.variant == COMEM_VARIANT_MFMA || (p.cfg.variant == COMEM_VARIANT_AUTO && bf16);
-  comem::KernelFn fn = use_mfma ? comem::select_mfma_kernel(p.cfg.head_dim, paged)
-                                : comem::select_valu_kernel(bf16, p.cfg.head_dim, group_of(p.cfg), paged);
+  comem::KernelFn fn = uses_mfma(p) ? comem::select_mfma_kernel(p.cfg.head_dim, paged, a.page_mask + 1)
+                                    : comem::select_valu_kernel(bf16, p.cfg.head_dim, group_of(p.cfg), paged);
   if (fn == nullptr) return COMEM_ERR_UNSUPPORTED;
   dim3 grid(static_cast<unsigned>(splits), static_cast<unsigned>(p.cfg.num_kv_heads),
             static_cast<unsigned>(batch));
@@ -303,6 +309,8 @@ comem_status comem_decode_attn_paged(const comem_decode_attn_plan* plan, const v
   int64_t chunk = 0, splits = 0;
   st = plan_call(*p, batch, max_ctx_len, workspace == nullptr ? 0 : workspace_bytes, &chunk, &splits);
   if (st != COMEM_OK) return st;
+  // The matrix-core kernel stages one split's block-table entries in LDS.
+  if (uses_mfma(*p) && (chunk - 1) / page_size + 2 > comem::mfma_max_split_pages()) return COMEM_ERR_INVALID_SHAPE;
   if (p->device == COMEM_NO_DEVICE) return COMEM_ERR_NO_DEVICE;
   comem::AttnParams a;
   fill_common(*p, a, q, k_pages, v_pages, stride_token, stride_head, ctx_lens, out, lse, workspace, batch,

@@ -20,6 +20,8 @@
 
 namespace comem {
 
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+
 constexpr int kWaves = 4;           // waves per workgroup
 constexpr int kThreads = 64 * kWaves;
 constexpr int kMaxGroup = 16;       // largest GQA group handled in one workgroup
@@ -86,17 +88,54 @@ __device__ inline float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
 // Partial results cross workgroups that may run on different XCDs, whose L2
 // caches are not coherent with each other. They are written and read with
-// device-scope accesses (relaxed atomics at agent scope: stores write through
-// to the device coherence point, loads bypass any stale cached copy), so no
+// device-scope accesses (the sc1 cache policy: stores write through to the
+// device coherence point, loads do not hit stale cached copies), so no
 // cache-wide writeback or invalidate is needed. A writer waits until its
 // stores are acknowledged before the workgroup takes its ticket.
-__device__ inline void store_coherent(float* p, float v) {
-  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+constexpr int kDeviceScope = 16;           // buffer-instruction cache policy bits: sc1
+constexpr int kBufferConfig = 0x00020000;  // buffer descriptor word 3 for raw buffers on CDNA
+
+__device__ inline __amdgpu_buffer_rsrc_t buffer_rsrc(const void* base, int bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, bytes, kBufferConfig);
 }
-__device__ inline float load_coherent(const float* p) {
-  return __hip_atomic_load(const_cast<float*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+__device__ inline void store4_coherent(__amdgpu_buffer_rsrc_t r, uint32_t off, float4 v) {
+  __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4_t, v), r, off, 0, kDeviceScope);
+}
+__device__ inline float4 load4_coherent(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+  return __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, kDeviceScope));
+}
+__device__ inline void store_coherent(__amdgpu_buffer_rsrc_t r, uint32_t off, float v) {
+  __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, v), r, off, 0, kDeviceScope);
+}
+__device__ inline float load_coherent(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, off, 0, kDeviceScope));
 }
 __device__ inline void wait_stores_done() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+
+// Online log-sum-exp merge state: running max m (log2 units), weight sum and
+// weighted sum of 4 output values. Merging is order-dependent only through
+// rounding; callers always merge in split order.
+struct MergeState {
+  float m = -INFINITY;
+  float wsum = 0.f;
+  float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+
+  // Add a part whose values o and weight sum wt are relative to 2^m2. A part
+  // with m2 = -inf adds nothing. Branch-free, so that callers' loads of
+  // later parts can be issued ahead of earlier merges.
+  __device__ void add(float m2, float wt, float4 o) {
+    const float mn = fmaxf(m, m2);
+    const float ref = mn == -INFINITY ? 0.f : mn;
+    const float a = fast_exp2(m - ref);
+    const float b = fast_exp2(m2 - ref);
+    acc.x = acc.x * a + b * o.x;
+    acc.y = acc.y * a + b * o.y;
+    acc.z = acc.z * a + b * o.z;
+    acc.w = acc.w * a + b * o.w;
+    wsum = wsum * a + b * wt;
+    m = mn;
+  }
+};
 
 // Merge the workgroup's wave states, write the split's result, and if this
 // split is the last of its (b, hk) to finish, merge all splits of (b, hk).
@@ -111,32 +150,30 @@ __device__ void finalize_split(const AttnParams& p, const WaveState<D>& ws, int 
   const int head0 = b * p.num_q_heads + hk * G;  // first query head row of this (b, hk)
   const bool single = nsplit_b == 1;
   const int64_t part0 = (static_cast<int64_t>(b) * p.num_kv_heads + hk) * p.num_splits;
+  // This (b, hk)'s partial results: lse [S][G] and outputs [S][G][D].
+  const __amdgpu_buffer_rsrc_t rl = buffer_rsrc(p.lse_part + part0 * G, nsplit_b * G * 4);
+  const __amdgpu_buffer_rsrc_t ro = buffer_rsrc(p.o_part + part0 * G * D, nsplit_b * G * D * 4);
+  const int slots = G * D / 4;  // 4 head_dim values per slot
 
-  for (int idx = tid; idx < G * D; idx += kThreads) {
-    const int h = idx / D;
-    const int d = idx - h * D;
-    float M = -INFINITY;
+  for (int slot = tid; slot < slots; slot += kThreads) {
+    const int h = (slot * 4) / D;
+    const int d0 = slot * 4 - h * D;
+    MergeState st;
 #pragma unroll
-    for (int w = 0; w < kWaves; ++w) M = fmaxf(M, ws.m[w][h]);
-    float o = 0.f, lt = 0.f;
-    if (M > -INFINITY) {
-#pragma unroll
-      for (int w = 0; w < kWaves; ++w) {
-        const float a = fast_exp2(ws.m[w][h] - M);  // exp2(-inf) = 0 for idle waves
-        o += a * ws.o[w][h][d];
-        lt += a * ws.l[w][h];
-      }
+    for (int w = 0; w < kWaves; ++w) {
+      const float4 o = *reinterpret_cast<const float4*>(&ws.o[w][h][d0]);
+      st.add(ws.m[w][h], ws.l[w][h], o);  // wave sums are unnormalised: weight 2^m, sum l
     }
-    const bool live = lt > 0.f;
-    const float on = live ? o / lt : 0.f;
-    const float lse2 = live ? M + log2f(lt) : -INFINITY;
+    const bool live = st.wsum > 0.f;
+    const float inv = live ? 1.f / st.wsum : 0.f;
+    const float4 on = make_float4(st.acc.x * inv, st.acc.y * inv, st.acc.z * inv, st.acc.w * inv);
+    const float lse2 = live ? st.m + log2f(st.wsum) : -INFINITY;
     if (single) {
-      p.out[static_cast<int64_t>(head0 + h) * D + d] = on;
-      if (d == 0 && p.lse != nullptr) p.lse[head0 + h] = live ? lse2 * kLn2 : -INFINITY;
+      *reinterpret_cast<float4*>(p.out + static_cast<int64_t>(head0 + h) * D + d0) = on;
+      if (d0 == 0 && p.lse != nullptr) p.lse[head0 + h] = live ? lse2 * kLn2 : -INFINITY;
     } else {
-      const int64_t slot = (part0 + j) * G + h;
-      store_coherent(&p.o_part[slot * D + d], on);
-      if (d == 0) store_coherent(&p.lse_part[slot], lse2);
+      store4_coherent(ro, ((j * G + h) * D + d0) * 4, on);
+      if (d0 == 0) store_coherent(rl, (j * G + h) * 4, lse2);
     }
   }
   if (single) return;
@@ -152,57 +189,42 @@ __device__ void finalize_split(const AttnParams& p, const WaveState<D>& ws, int 
   if (!sm_last) return;
   if (tid == 0) atomicExch(&p.tickets[b * p.num_kv_heads + hk], 0u);
 
-  // Per-head maximum of the split lse values. G divides kThreads, so thread
-  // tid only ever reads head tid % G; partial maxima meet in LDS.
-  __shared__ float sm_red[kThreads];
-  __shared__ float sm_max[kMaxGroup];
-  const float* lp = p.lse_part + part0 * G;
-  {
-    float mloc = -INFINITY;
-    for (int idx = tid; idx < nsplit_b * G; idx += kThreads) mloc = fmaxf(mloc, load_coherent(lp + idx));
-    sm_red[tid] = mloc;
-  }
-  __syncthreads();
-  if (tid < G) {
-    float M = -INFINITY;
-    for (int i = tid; i < kThreads; i += G) M = fmaxf(M, sm_red[i]);
-    sm_max[tid] = M;
-  }
-  __syncthreads();
-
-  // Weighted sum over splits, 4 head_dim values per slot. When there are
-  // fewer slots than threads, tps threads share a slot, taking splits
-  // sub, sub + tps, ...; their sums are then added in sub order.
-  const int slots = G * D / 4;
+  // Merge over splits in one pass. When there are fewer slots than threads,
+  // tps threads share a slot, taking splits sub, sub + tps, ...; their states
+  // are then merged in sub order. Each split part has weight sum 1 (it is
+  // normalised) and log-weight lse2.
   const int tps = slots >= kThreads ? 1 : kThreads / slots;
   __shared__ float4 sm_acc[kThreads];
-  __shared__ float sm_wsum[kThreads];
+  __shared__ float sm_m[kThreads];
+  __shared__ float sm_w[kThreads];
   for (int slot = tid / tps; slot < slots; slot += kThreads / tps) {
     const int sub = tid % tps;
     const int h = (slot * 4) / D;
     const int d0 = slot * 4 - h * D;
-    const float M = sm_max[h];
-    const float* op = p.o_part + (part0 * G + h) * D + d0;
-    float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
-    float wsum = 0.f;
-#pragma unroll 8
-    for (int s = sub; s < nsplit_b; s += tps) {
-      const float w = fast_exp2(load_coherent(lp + static_cast<int64_t>(s) * G + h) - M);
-      const float* o = op + static_cast<int64_t>(s) * G * D;
-      acc.x += w * load_coherent(o);
-      acc.y += w * load_coherent(o + 1);
-      acc.z += w * load_coherent(o + 2);
-      acc.w += w * load_coherent(o + 3);
-      wsum += w;
+    MergeState st;
+    // Batches of 8 splits: all 16 loads of a batch are in flight together.
+    // Indices past the last split re-read the last one and get weight 0.
+    for (int s0 = sub; s0 < nsplit_b; s0 += 8 * tps) {
+      float l2[8];
+      float4 o[8];
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        const int si = min(s0 + i * tps, nsplit_b - 1);
+        l2[i] = load_coherent(rl, (si * G + h) * 4);
+        o[i] = load4_coherent(ro, ((si * G + h) * D + d0) * 4);
+      }
+#pragma unroll
+      for (int i = 0; i < 8; ++i) st.add(s0 + i * tps < nsplit_b ? l2[i] : -INFINITY, 1.f, o[i]);
     }
     if (tps == 1) {
-      const float inv = 1.f / wsum;
+      const float inv = 1.f / st.wsum;
       *reinterpret_cast<float4*>(p.out + static_cast<int64_t>(head0 + h) * D + d0) =
-          make_float4(acc.x * inv, acc.y * inv, acc.z * inv, acc.w * inv);
-      if (d0 == 0 && p.lse != nullptr) p.lse[head0 + h] = (M + log2f(wsum)) * kLn2;
+          make_float4(st.acc.x * inv, st.acc.y * inv, st.acc.z * inv, st.acc.w * inv);
+      if (d0 == 0 && p.lse != nullptr) p.lse[head0 + h] = (st.m + log2f(st.wsum)) * kLn2;
     } else {
-      sm_acc[tid] = acc;
-      sm_wsum[tid] = wsum;
+      sm_acc[tid] = st.acc;
+      sm_m[tid] = st.m;
+      sm_w[tid] = st.wsum;
     }
   }
   if (tps == 1) return;
@@ -211,20 +233,12 @@ __device__ void finalize_split(const AttnParams& p, const WaveState<D>& ws, int 
     const int slot = tid / tps;
     const int h = (slot * 4) / D;
     const int d0 = slot * 4 - h * D;
-    float4 acc = sm_acc[tid];
-    float wsum = sm_wsum[tid];
-    for (int i = 1; i < tps; ++i) {
-      const float4 o = sm_acc[tid + i];
-      acc.x += o.x;
-      acc.y += o.y;
-      acc.z += o.z;
-      acc.w += o.w;
-      wsum += sm_wsum[tid + i];
-    }
-    const float inv = 1.f / wsum;
+    MergeState st;
+    for (int i = 0; i < tps; ++i) st.add(sm_m[tid + i], sm_w[tid + i], sm_acc[tid + i]);
+    const float inv = 1.f / st.wsum;
     *reinterpret_cast<float4*>(p.out + static_cast<int64_t>(head0 + h) * D + d0) =
-        make_float4(acc.x * inv, acc.y * inv, acc.z * inv, acc.w * inv);
-    if (d0 == 0 && p.lse != nullptr) p.lse[head0 + h] = (sm_max[h] + log2f(wsum)) * kLn2;
+        make_float4(st.acc.x * inv, st.acc.y * inv, st.acc.z * inv, st.acc.w * inv);
+    if (d0 == 0 && p.lse != nullptr) p.lse[head0 + h] = (st.m + log2f(st.wsum)) * kLn2;
   }
 }
 

@@ -45,11 +45,17 @@ template <>
 struct VRow<128> {
   u32x4 w;
   __device__ uint32_t word(int i) const { return w[i]; }
+  __device__ void load(__amdgpu_buffer_rsrc_t r, uint32_t voff, int soff) {
+    w = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0));
+  }
 };
 template <>
 struct VRow<64> {
   u32x2 w;
   __device__ uint32_t word(int i) const { return w[i]; }
+  __device__ void load(__amdgpu_buffer_rsrc_t r, uint32_t voff, int soff) {
+    w = __builtin_bit_cast(u32x2, __builtin_amdgcn_raw_buffer_load_b64(r, voff, soff, 0));
+  }
 };
 
 template <int D>
@@ -61,50 +67,73 @@ struct Tile {
 
 __device__ inline bf16x8 as_bf16x8(u32x4 x) { return __builtin_bit_cast(bf16x8, x); }
 
-template <int D, bool PAGED>
-struct MfmaCtx {
-  const AttnParams& p;
-  const char* kb;  // K base for this (hk)
-  const char* vb;
-  int b;
-  int64_t seq0;
+// Page lookups of one split go through LDS: the workgroup copies the split's
+// block-table entries there once, so the token loop never waits on them.
+constexpr int kMaxSplitPages = 2048;
+
+enum class Layout { kContig, kPaged, kPagedFine };
+
+template <int D, Layout LAYOUT>
+struct Loader {
+  const char* kbase;  // K of this (b, hk): contiguous layout already offset to the sequence start
+  const char* vbase;
+  const int32_t* sm_pages;  // LDS copy of the split's block-table entries (paged layouts)
+  int page_first;           // token index of the first entry in sm_pages
+  int64_t stride_token;
+  int64_t stride_page;
+  int page_shift, page_mask;
   int t_end;
   int c, g;
-  int64_t k_lane;     // c * stride_token
-  int64_t v_lane[4];  // (4g + r) * stride_token
+  uint32_t koff;  // c * stride_token + 16 g
+  uint32_t voff;  // 4 g * stride_token + 2 * NT * c
 
-  __device__ void load(Tile<D>& T, int t0) const {
-    constexpr int KB = D / 32;
-    constexpr int VBYTES = D / 8;  // bytes of one lane's V slice (NT bf16)
-    const bool full = (t0 + 32 <= t_end) && (!PAGED || p.page_shift >= 4);
-    if (full) {
-#pragma unroll
-      for (int s = 0; s < 2; ++s) {
-        const int64_t base = uniform_i64(row_offset<PAGED>(p, b, seq0, t0 + 16 * s));
-        const char* kr = kb + base + k_lane + 16 * g;
-#pragma unroll
-        for (int kk = 0; kk < KB; ++kk) T.k[s][kk] = *reinterpret_cast<const u32x4*>(kr + 64 * kk);
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const char* vr = vb + base + v_lane[r] + VBYTES * c;
-          T.v[s][r].w = *reinterpret_cast<const decltype(T.v[s][r].w)*>(vr);
-        }
-      }
+  // Byte offset of token t from the base; uniform across the wave when t is.
+  __device__ int64_t token_offset(int t) const {
+    if constexpr (LAYOUT == Layout::kContig) {
+      return static_cast<int64_t>(t) * stride_token;
     } else {
-      // Partial tile (or pages shorter than a sub-tile): per-lane rows, with
-      // tokens past the end clamped to the last valid row (their weight is 0).
+      const int page = sm_pages[(t - page_first) >> page_shift];
+      return static_cast<int64_t>(page) * stride_page + static_cast<int64_t>(t & page_mask) * stride_token;
+    }
+  }
+
+  // A full 32-token tile whose 16-token halves each lie in one page (or the
+  // contiguous layout): per half, one buffer descriptor on the half's first
+  // row (uniform, in SGPRs) and fixed 32-bit lane offsets. The descriptor's
+  // size covers exactly the 16 rows, so the hardware returns zeros instead of
+  // touching memory should an offset ever fall outside them.
+  __device__ void load_full(Tile<D>& T, int t0) const {
+    constexpr int KB = D / 32;
+    const int extent = static_cast<int>(15 * stride_token + 2 * D);
 #pragma unroll
-      for (int s = 0; s < 2; ++s) {
-        const int tk = min(t0 + 16 * s + c, t_end - 1);
-        const char* kr = kb + row_offset<PAGED>(p, b, seq0, tk) + 16 * g;
+    for (int s = 0; s < 2; ++s) {
+      const int64_t base = uniform_i64(token_offset(t0 + 16 * s));
+      const __amdgpu_buffer_rsrc_t rk =
+          __builtin_amdgcn_make_buffer_rsrc(const_cast<char*>(kbase + base), 0, extent, kBufferConfig);
+      const __amdgpu_buffer_rsrc_t rv =
+          __builtin_amdgcn_make_buffer_rsrc(const_cast<char*>(vbase + base), 0, extent, kBufferConfig);
 #pragma unroll
-        for (int kk = 0; kk < KB; ++kk) T.k[s][kk] = *reinterpret_cast<const u32x4*>(kr + 64 * kk);
+      for (int kk = 0; kk < KB; ++kk)
+        T.k[s][kk] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rk, koff + 64 * kk, 0, 0));
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int tv = min(t0 + 16 * s + 4 * g + r, t_end - 1);
-          const char* vr = vb + row_offset<PAGED>(p, b, seq0, tv) + VBYTES * c;
-          T.v[s][r].w = *reinterpret_cast<const decltype(T.v[s][r].w)*>(vr);
-        }
+      for (int r = 0; r < 4; ++r) T.v[s][r].load(rv, voff, static_cast<int>(r * stride_token));
+    }
+  }
+
+  // Any tile: per-lane rows; tokens past the end are clamped to the last
+  // valid row (their weight is zero), so no byte outside a context is read.
+  __device__ void load_any(Tile<D>& T, int t0) const {
+    constexpr int KB = D / 32;
+    constexpr int VBYTES = D / 8;
+#pragma unroll
+    for (int s = 0; s < 2; ++s) {
+      const char* kr = kbase + token_offset(min(t0 + 16 * s + c, t_end - 1)) + 16 * g;
+#pragma unroll
+      for (int kk = 0; kk < KB; ++kk) T.k[s][kk] = *reinterpret_cast<const u32x4*>(kr + 64 * kk);
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const char* vr = vbase + token_offset(min(t0 + 16 * s + 4 * g + r, t_end - 1)) + VBYTES * c;
+        T.v[s][r].w = *reinterpret_cast<const decltype(T.v[s][r].w)*>(vr);
       }
     }
   }
@@ -141,7 +170,7 @@ __device__ inline void compute_tile(const Tile<D>& T, int t0, int t_end, int c, 
   // Every tile holds at least one valid token, so m_new is finite.
   const float m_new = fmaxf(m_run, mt);
   const float alpha = fast_exp2(m_run - m_new);
-  if (__any(m_new > m_run)) {
+  {
     float ar[4];
 #pragma unroll
     for (int r = 0; r < 4; ++r) ar[r] = __shfl(alpha, 4 * g + r);
@@ -184,7 +213,7 @@ __device__ inline void compute_tile(const Tile<D>& T, int t0, int t_end, int c, 
   }
 }
 
-template <int D, bool PAGED>
+template <int D, Layout LAYOUT>
 __global__ __launch_bounds__(kThreads, 2) void decode_mfma_kernel(const AttnParams p) {
   constexpr int KB = D / 32;
   constexpr int NT = D / 16;
@@ -194,11 +223,40 @@ __global__ __launch_bounds__(kThreads, 2) void decode_mfma_kernel(const AttnPara
   if (j >= nsplit_b) return;
   const int t_begin = j * p.chunk;
   const int t_end = t_begin + min(L - t_begin, p.chunk);
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63;
+  const int w = uniform_i32(threadIdx.x >> 6);
   const int c = lane & 15, g = lane >> 4;
   const int G = p.group;
 
   __shared__ WaveState<D> ws;
+  __shared__ int32_t sm_pages[LAYOUT == Layout::kContig ? 1 : kMaxSplitPages];
+
+  Loader<D, LAYOUT> ld;
+  ld.kbase = p.k + hk * p.stride_head;
+  ld.vbase = p.v + hk * p.stride_head;
+  if constexpr (LAYOUT == Layout::kContig) {
+    const int64_t seq0 = p.seq_start[b] * p.stride_token;
+    ld.kbase += seq0;
+    ld.vbase += seq0;
+  } else {
+    // Entries for tokens [t_begin, t_end); never past ceil(L / page_size).
+    ld.page_first = t_begin & ~p.page_mask;
+    const int first = t_begin >> p.page_shift;
+    const int count = ((t_end - 1) >> p.page_shift) - first + 1;
+    const int32_t* row = p.block_table + static_cast<int64_t>(b) * p.max_pages + first;
+    for (int i = threadIdx.x; i < count; i += kThreads) sm_pages[i] = row[i];
+    __syncthreads();
+  }
+  ld.sm_pages = sm_pages;
+  ld.stride_token = p.stride_token;
+  ld.stride_page = p.stride_page;
+  ld.page_shift = p.page_shift;
+  ld.page_mask = p.page_mask;
+  ld.t_end = t_end;
+  ld.c = c;
+  ld.g = g;
+  ld.koff = static_cast<uint32_t>(c * p.stride_token + 16 * g);
+  ld.voff = static_cast<uint32_t>(4 * g * p.stride_token + 2 * NT * c);
 
   // Q operand: head c of the group (zero columns past G), slice 32kb + 8g.
   bf16x8 qop[KB];
@@ -212,30 +270,49 @@ __global__ __launch_bounds__(kThreads, 2) void decode_mfma_kernel(const AttnPara
     }
   }
 
-  MfmaCtx<D, PAGED> ctx{p, p.k + hk * p.stride_head, p.v + hk * p.stride_head, b,
-                        PAGED ? 0 : p.seq_start[b], t_end, c, g, c * p.stride_token, {}};
-#pragma unroll
-  for (int r = 0; r < 4; ++r) ctx.v_lane[r] = (4 * g + r) * p.stride_token;
-
   float m_run = -INFINITY, l_run = 0.f;
   f32x4 acc[NT];
 #pragma unroll
   for (int n = 0; n < NT; ++n) acc[n] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  const int ntiles = (t_end - t_begin + 31) / 32;
+  const int ntok = t_end - t_begin;
+  const int nfull = ntok >> 5;              // full 32-token tiles
+  const int ntiles = (ntok + 31) >> 5;      // including a partial last tile
   int ti = w;
-  if (ti < ntiles) {
-    Tile<D> A, B;
-    ctx.load(A, t_begin + 32 * ti);
-    while (true) {
-      if (ti + kWaves < ntiles) ctx.load(B, t_begin + 32 * (ti + kWaves));
+  if constexpr (LAYOUT != Layout::kPagedFine) {
+    // Full tiles w, w + 4, ...: while one tile is computed the next is in
+    // flight. The prefetch is issued unconditionally (past the last full tile
+    // it re-reads the current one, which is still cached) and pinned ahead of
+    // the compute, so the compiler waits for exactly the older tile's loads.
+    if (ti < nfull) {
+      Tile<D> A, B;
+      ld.load_full(A, t_begin + 32 * ti);
+      for (;;) {
+        int nx = ti + kWaves;
+        ld.load_full(B, t_begin + 32 * (nx < nfull ? nx : ti));
+        __builtin_amdgcn_sched_barrier(0);
+        compute_tile<D>(A, t_begin + 32 * ti, t_end, c, g, qop, p.scale_log2, m_run, l_run, acc);
+        if (nx >= nfull) break;
+        ti = nx;
+        nx = ti + kWaves;
+        ld.load_full(A, t_begin + 32 * (nx < nfull ? nx : ti));
+        __builtin_amdgcn_sched_barrier(0);
+        compute_tile<D>(B, t_begin + 32 * ti, t_end, c, g, qop, p.scale_log2, m_run, l_run, acc);
+        if (nx >= nfull) break;
+        ti = nx;
+      }
+    }
+    ti = nfull;  // the partial tile, if any, belongs to wave nfull % kWaves
+    if (ti < ntiles && (ti % kWaves) == w) {
+      Tile<D> A;
+      ld.load_any(A, t_begin + 32 * ti);
       compute_tile<D>(A, t_begin + 32 * ti, t_end, c, g, qop, p.scale_log2, m_run, l_run, acc);
-      ti += kWaves;
-      if (ti >= ntiles) break;
-      if (ti + kWaves < ntiles) ctx.load(A, t_begin + 32 * (ti + kWaves));
-      compute_tile<D>(B, t_begin + 32 * ti, t_end, c, g, qop, p.scale_log2, m_run, l_run, acc);
-      ti += kWaves;
-      if (ti >= ntiles) break;
+    }
+  } else {
+    for (; ti < ntiles; ti += kWaves) {
+      Tile<D> A;
+      ld.load_any(A, t_begin + 32 * ti);
+      compute_tile<D>(A, t_begin + 32 * ti, t_end, c, g, qop, p.scale_log2, m_run, l_run, acc);
     }
   }
 
@@ -262,10 +339,18 @@ __global__ __launch_bounds__(kThreads, 2) void decode_mfma_kernel(const AttnPara
 
 using KernelFn = void (*)(AttnParams);
 
-KernelFn select_mfma_kernel(int head_dim, bool paged) {
-  if (head_dim == 128) return paged ? decode_mfma_kernel<128, true> : decode_mfma_kernel<128, false>;
-  if (head_dim == 64) return paged ? decode_mfma_kernel<64, true> : decode_mfma_kernel<64, false>;
+template <int D>
+KernelFn pick_layout(bool paged, int page_size) {
+  if (!paged) return decode_mfma_kernel<D, Layout::kContig>;
+  return page_size >= 16 ? decode_mfma_kernel<D, Layout::kPaged> : decode_mfma_kernel<D, Layout::kPagedFine>;
+}
+
+KernelFn select_mfma_kernel(int head_dim, bool paged, int page_size) {
+  if (head_dim == 128) return pick_layout<128>(paged, page_size);
+  if (head_dim == 64) return pick_layout<64>(paged, page_size);
   return nullptr;
 }
+
+int mfma_max_split_pages() { return kMaxSplitPages; }
 
 }  // namespace comem
