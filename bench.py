@@ -16,6 +16,9 @@ oracle timed on a bounded sample as a reported baseline.
 from __future__ import annotations
 
 import argparse
+import csv
+import glob
+import hashlib
 import json
 import math
 import os
@@ -28,6 +31,10 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 PEAK_HBM_GBPS = 8000.0
+PROFILES = os.path.join(ROOT, "profiles")
+KERNEL_SOURCES = ["paper_2605_30842_amd/csrc/api.cpp", "paper_2605_30842_amd/csrc/attn_common.h",
+                  "paper_2605_30842_amd/csrc/kernel_mfma.hip", "paper_2605_30842_amd/csrc/kernel_valu.hip"]
+COPY_CAL_BYTES = 256 << 20  # size of the copy used to calibrate FETCH_SIZE / WRITE_SIZE
 METRIC = "decode-attention effective HBM GB/s (% of peak) and µs/step at 32k-128k ctx"
 MALL_BYTES = 256 << 20
 
@@ -38,13 +45,179 @@ def _args():
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--workload", type=int, default=2, help="named workload 1..5 (2 = the headline one)")
-    ap.add_argument("--variant", default="auto", choices=["auto", "mfma", "valu"])
+    ap.add_argument("--variant", default="auto", choices=["auto", "mfma", "mfma_grid", "valu"])
     ap.add_argument("--chunk", type=int, default=0, help="tokens per split (0 = planned)")
     ap.add_argument("--copies", type=int, default=0, help="KV copies to cycle over (0 = enough to exceed the LLC)")
     ap.add_argument("--cpu-seconds", type=float, default=10.0, help="budget of the CPU oracle baseline (0 = skip)")
     ap.add_argument("--timing", default="graph", choices=["graph", "eager"],
                     help="graph: replay captured launches (no host launch cost in the timed region)")
+    ap.add_argument("--probe", choices=["read", "copy"], default=None,
+                    help="instead of attention, time the streaming-read or copy probe kernel")
+    ap.add_argument("--probe-bytes", type=int, default=4 << 30)
+    ap.add_argument("--probe-blocks", type=int, default=4096)
+    ap.add_argument("--summarize", metavar="DIR", default=None,
+                    help="write profiles/ summaries from rocprofv3 outputs under DIR (see profiles/README.md)")
     return ap.parse_args()
+
+
+def kernel_source_hash() -> str:
+    h = hashlib.sha256()
+    for rel in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, rel), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def _counter_medians(path):
+    """Median per counter over dispatches of the attention kernel (or of the copy probe)."""
+    vals = {}
+    for f in glob.glob(os.path.join(path, "**", "*counter_collection.csv"), recursive=True):
+        for r in csv.DictReader(open(f)):
+            k = r["Kernel_Name"]
+            kind = "attn" if "decode_" in k else ("copy" if "copy_kernel" in k else None)
+            if kind:
+                vals.setdefault((kind, r["Counter_Name"]), []).append(float(r["Counter_Value"]))
+    return {k: sorted(v)[len(v) // 2] for k, v in vals.items()}
+
+
+def _short_kernel_name(full):
+    """decode_mfma_queue_kernel<128, Layout 1> -> decode_mfma_queue_D128_paged (and similar)."""
+    import re
+
+    m = re.search(r"(decode_\w+?)(?:_kernel)?<([^>]*)>", full)
+    if not m:
+        return re.sub(r"\W+", "_", full.split("<")[0]).strip("_")[:60]
+    base, args = m.group(1), m.group(2)
+    parts = [x.strip() for x in re.split(r",\s*(?![^()]*\))", args)]
+    name = base
+    for a in parts:
+        lay = re.search(r"Layout\)(\d)", a)
+        if lay:
+            name += "_" + ["contig", "paged", "pagedfine"][int(lay.group(1))]
+        elif a.isdigit():
+            name += f"_D{a}" if a in ("64", "128") else f"_{a}"
+        elif "Bf16" in a:
+            name += "_bf16"
+        elif a == "float":
+            name += "_f32"
+        elif a in ("true", "false"):
+            name += "_paged" if a == "true" else "_contig"
+    return name
+
+
+def _kernel_stats(path):
+    rows = []
+    for f in glob.glob(os.path.join(path, "**", "*kernel_stats.csv"), recursive=True):
+        rows += list(csv.DictReader(open(f)))
+    return rows
+
+
+def summarize(a):
+    """profiles/<kernel>_<workload>.md from the rocprofv3 runs under DIR.
+
+    Expected layout (each made by the command shown in the summary):
+      DIR/prof/w<N>/   --kernel-trace --stats of the default bench run of workload N
+      DIR/pmc/w<N>_fetch, DIR/pmc/w<N>_write   FETCH_SIZE / WRITE_SIZE runs of workload N
+      DIR/pmc/copy_fetch, DIR/pmc/copy_write   the same counters on a 256 MiB copy
+    """
+    from workloads.synth import WORKLOADS, generate
+
+    d = a.summarize
+    cal_f = _counter_medians(os.path.join(d, "pmc", "copy_fetch")).get(("copy", "FETCH_SIZE"))
+    cal_w = _counter_medians(os.path.join(d, "pmc", "copy_write")).get(("copy", "WRITE_SIZE"))
+    fetch_scale = COPY_CAL_BYTES / 1024 / cal_f if cal_f else None
+    write_scale = COPY_CAL_BYTES / 1024 / cal_w if cal_w else None
+    os.makedirs(PROFILES, exist_ok=True)
+    for i, spec in WORKLOADS.items():
+        stats = _kernel_stats(os.path.join(d, "prof", f"w{i}"))
+        if not stats:
+            continue
+        attn = [r for r in stats if "decode_" in r["Name"]]
+        w = generate(spec)
+        kv = w.kv_bytes
+        fm = _counter_medians(os.path.join(d, "pmc", f"w{i}_fetch")).get(("attn", "FETCH_SIZE"))
+        wm = _counter_medians(os.path.join(d, "pmc", f"w{i}_write")).get(("attn", "WRITE_SIZE"))
+        traffic = None
+        if fm and wm and fetch_scale and write_scale:
+            traffic = round(fm * 1024 * fetch_scale + wm * 1024 * write_scale)
+        kname = _short_kernel_name(attn[0]["Name"]) if attn else "none"
+        avg_ns = float(attn[0]["AverageNs"]) if attn else None
+        rec = {"workload": spec.name, "kernel": kname, "kernel_source_hash": kernel_source_hash(),
+               "calls": int(attn[0]["Calls"]) if attn else 0, "avg_duration_us": avg_ns / 1e3 if avg_ns else None,
+               "algorithmic_bytes": kv, "achieved_GBps_from_trace": round(kv / avg_ns, 1) if avg_ns else None,
+               "fetch_KiB_per_dispatch": fm, "write_KiB_per_dispatch": wm,
+               "fetch_scale": fetch_scale, "write_scale": write_scale, "traffic_bytes": traffic,
+               "traffic_over_algorithmic": round(traffic / kv, 4) if traffic else None}
+        name = f"{kname}_{spec.name}.md"
+        with open(os.path.join(PROFILES, name), "w") as f:
+            f.write(f"# {kname} on {spec.name}\n\n")
+            f.write("Commands (run from the repository root on the MI355X box, after `cd /tmp && export TMPDIR=/tmp`"
+                    " and returning to the root):\n\n```\n")
+            f.write(f"rocprofv3 --kernel-trace --stats --output-format csv -d {d}/prof/w{i} -o w{i} -- "
+                    f"python bench.py --workload {i} --cpu-seconds 0\n")
+            for c in ("FETCH_SIZE", "WRITE_SIZE"):
+                sub = "fetch" if c == "FETCH_SIZE" else "write"
+                f.write(f"rocprofv3 --pmc {c} --output-format csv -d {d}/pmc/w{i}_{sub} -o w{i}_{sub} -- "
+                        f"python bench.py --workload {i} --timing eager --steps 4 --warmup 1 --cpu-seconds 0\n")
+                f.write(f"rocprofv3 --pmc {c} --output-format csv -d {d}/pmc/copy_{sub} -o copy_{sub} -- "
+                        f"python bench.py --probe copy --probe-bytes {COPY_CAL_BYTES} --steps 3 --warmup 1\n")
+            f.write(f"python bench.py --summarize {d}\n```\n\n")
+            f.write("Kernel statistics (rocprofv3 --stats, all dispatches of the bench run):\n\n")
+            f.write("| kernel | calls | avg us | min us | max us |\n|---|---|---|---|---|\n")
+            for r in stats:
+                f.write(f"| {_short_kernel_name(r['Name'])} | {r['Calls']} | {float(r['AverageNs'])/1e3:.2f} | "
+                        f"{float(r['MinNs'])/1e3:.2f} | {float(r['MaxNs'])/1e3:.2f} |\n")
+            f.write("\nHBM traffic per dispatch: FETCH_SIZE and WRITE_SIZE medians (KiB), each scaled by the factor "
+                    f"that makes the same counter read {COPY_CAL_BYTES} bytes for a copy of that size.\n\n")
+            f.write("```json\n" + json.dumps(rec, indent=1) + "\n```\n")
+        print(f"wrote profiles/{name}", flush=True)
+
+
+def recorded_traffic(workload_name):
+    """HBM bytes per dispatch from a profiles/ summary of the current kernel sources, else None."""
+    for f in glob.glob(os.path.join(PROFILES, f"*_{workload_name}.md")):
+        txt = open(f).read()
+        if "```json" not in txt:
+            continue
+        rec = json.loads(txt.split("```json", 1)[1].split("```", 1)[0])
+        if rec.get("kernel_source_hash") == kernel_source_hash() and rec.get("traffic_bytes"):
+            return rec["traffic_bytes"]
+    return None
+
+
+def _probe(a):
+    """Streaming read (practical HBM read ceiling) or copy (profiler byte-counter calibration)."""
+    import torch
+
+    from paper_2605_30842_amd import binding
+
+    binding.load_probe_library()
+    n = a.probe_bytes
+    src = torch.ones(n // 4, dtype=torch.int32, device="cuda")
+    dst = torch.empty_like(src) if a.probe == "copy" else None
+    sink = torch.zeros(256 * a.probe_blocks, dtype=torch.int32, device="cuda")
+    stream = torch.cuda.current_stream()
+
+    def once():
+        if a.probe == "read":
+            binding.comem_probe_read(src.data_ptr(), n, sink.data_ptr(), a.probe_blocks, stream.cuda_stream)
+        else:
+            binding.comem_probe_copy(src.data_ptr(), dst.data_ptr(), n, a.probe_blocks, stream.cuda_stream)
+
+    for _ in range(a.warmup):
+        once()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(a.steps):
+        once()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / a.steps
+    moved = n * (2 if a.probe == "copy" else 1)
+    print(json.dumps({"probe": a.probe, "bytes": n, "bytes_moved": moved, "blocks": a.probe_blocks,
+                      "us_per_call": round(ms * 1e3, 3), "GB_per_s": round(moved / (ms * 1e-3) / 1e9, 1),
+                      "steps": a.steps}), flush=True)
 
 
 def _cpu_baseline(w, budget_s):
@@ -84,6 +257,12 @@ def main():
         print(f"bench.py runs on one GPU only (asked for --gpus {a.gpus}); this build has no multi-GPU path.",
               file=sys.stderr)
         sys.exit(2)
+    if a.probe:
+        _probe(a)
+        return
+    if a.summarize:
+        summarize(a)
+        return
     import torch
 
     from paper_2605_30842_amd import binding
@@ -164,7 +343,7 @@ def main():
     assert torch.isfinite(out).all().item()
 
     cpu = _cpu_baseline(w, a.cpu_seconds) if a.cpu_seconds > 0 else None
-    kind = "mfma" if (a.variant == "mfma" or (a.variant == "auto" and spec.dtype == "bf16")) else "valu"
+    kind = a.variant if a.variant != "auto" else ("mfma" if spec.dtype == "bf16" else "valu")
     line = {
         "metric": METRIC,
         "value": round(gbps, 2),
@@ -190,7 +369,7 @@ def main():
         },
         "roofline": {
             "bound": "hbm", "achieved": round(gbps, 2), "peak": PEAK_HBM_GBPS, "unit": "GB/s",
-            "frac": round(gbps / PEAK_HBM_GBPS, 4), "traffic": None,
+            "frac": round(gbps / PEAK_HBM_GBPS, 4), "traffic": recorded_traffic(spec.name),
         },
         "cpu_baseline": cpu,
     }

@@ -67,9 +67,12 @@ typedef enum {
 } comem_dtype;
 
 typedef enum {
-  COMEM_VARIANT_AUTO = 0, /* bf16 -> matrix-core kernel; f32 -> vector kernel */
-  COMEM_VARIANT_VALU = 1, /* vector-ALU kernel (f32 and bf16) */
-  COMEM_VARIANT_MFMA = 2  /* matrix-core kernel (bf16 only) */
+  COMEM_VARIANT_AUTO = 0,     /* bf16 -> matrix-core kernel; f32 -> vector kernel */
+  COMEM_VARIANT_VALU = 1,     /* vector-ALU kernel (f32 and bf16), one workgroup per split */
+  COMEM_VARIANT_MFMA = 2,     /* matrix-core kernel (bf16 only); persistent workgroups take
+                                 splits from a work queue when a workspace is given and
+                                 batch <= 4096, else one workgroup per split */
+  COMEM_VARIANT_MFMA_GRID = 3 /* matrix-core kernel, always one workgroup per split */
 } comem_variant;
 
 /* Pass as `device` to comem_decode_attn_init to make a plan without touching

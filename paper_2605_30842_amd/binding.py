@@ -17,17 +17,19 @@ from typing import Optional, Tuple
 
 PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(PKG, "libcomem_attn.so")
+PROBE_LIB_PATH = os.path.join(PKG, "libcomem_probe.so")
 
 OK, ERR_NULL_POINTER, ERR_INVALID_SHAPE, ERR_UNSUPPORTED, ERR_MISALIGNED = 0, 1, 2, 3, 4
 ERR_WORKSPACE_TOO_SMALL, ERR_BAD_HANDLE, ERR_HIP, ERR_NO_DEVICE = 5, 6, 7, 8
 F32, BF16 = 0, 1
-VARIANT_AUTO, VARIANT_VALU, VARIANT_MFMA = 0, 1, 2
+VARIANT_AUTO, VARIANT_VALU, VARIANT_MFMA, VARIANT_MFMA_GRID = 0, 1, 2, 3
 NO_DEVICE = -1
 
 EXPORTED = (
     "comem_decode_attn_init", "comem_decode_attn_destroy", "comem_status_string",
     "comem_decode_attn_plan_splits", "comem_decode_attn", "comem_decode_attn_paged",
 )
+PROBE_EXPORTED = ("comem_probe_read", "comem_probe_copy")
 
 
 class Config(ctypes.Structure):
@@ -78,6 +80,38 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.comem_decode_attn_paged.restype = ctypes.c_int
     _lib = lib
     return lib
+
+
+_probe = None
+
+
+def load_probe_library(path: str = PROBE_LIB_PATH) -> ctypes.CDLL:
+    """The measurement kernels (streaming read, copy); raise if not built."""
+    global _probe
+    if _probe is not None:
+        return _probe
+    if not os.path.exists(path):
+        raise RuntimeError(f"{path} not found: build it with `python -m paper_2605_30842_amd.build`")
+    lib = ctypes.CDLL(path)
+    vp, sz = ctypes.c_void_p, ctypes.c_size_t
+    lib.comem_probe_read.argtypes = [vp, sz, vp, ctypes.c_int, vp]
+    lib.comem_probe_read.restype = ctypes.c_int
+    lib.comem_probe_copy.argtypes = [vp, vp, sz, ctypes.c_int, vp]
+    lib.comem_probe_copy.restype = ctypes.c_int
+    _probe = lib
+    return lib
+
+
+def comem_probe_read(src, nbytes, sink, blocks, stream) -> None:
+    err = load_probe_library().comem_probe_read(src, nbytes, sink, blocks, stream)
+    if err != 0:
+        raise RuntimeError(f"comem_probe_read: HIP error {err}")
+
+
+def comem_probe_copy(src, dst, nbytes, blocks, stream) -> None:
+    err = load_probe_library().comem_probe_copy(src, dst, nbytes, blocks, stream)
+    if err != 0:
+        raise RuntimeError(f"comem_probe_copy: HIP error {err}")
 
 
 def status_string(status: int) -> str:
@@ -148,7 +182,8 @@ class DecodeAttention:
 
         self.cfg = Config(num_q_heads, num_kv_heads, head_dim, BF16 if dtype == "bf16" else F32, float(scale),
                           max_batch, max_ctx_len, chunk_tokens,
-                          {"auto": VARIANT_AUTO, "valu": VARIANT_VALU, "mfma": VARIANT_MFMA}[variant])
+                          {"auto": VARIANT_AUTO, "valu": VARIANT_VALU, "mfma": VARIANT_MFMA,
+                           "mfma_grid": VARIANT_MFMA_GRID}[variant])
         self.device = device
         self.plan, self.workspace_bytes = comem_decode_attn_init(self.cfg, device)
         self.workspace = torch.zeros(max(self.workspace_bytes, 256), dtype=torch.uint8, device=f"cuda:{device}")

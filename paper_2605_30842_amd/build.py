@@ -18,6 +18,8 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB_NAME = "libcomem_attn.so"
 SOURCES = ["api.cpp", "kernel_mfma.hip", "kernel_valu.hip"]
+PROBE_LIB_NAME = "libcomem_probe.so"
+PROBE_SOURCES = ["probe.hip"]
 ARCH = "gfx950"
 
 # Packed fp32 VALU instructions are kept out of the generated code.
@@ -48,13 +50,13 @@ def _run(cmd, verbose):
         print(err, file=sys.stderr)
 
 
-def build_library(out_dir: str = PKG, verbose: bool = False) -> str:
+def _build_one(name, sources, out_dir, verbose):
     hipcc = _hipcc()
     obj_dir = os.path.join(ROOT, "_build")
     os.makedirs(obj_dir, exist_ok=True)
     objs = []
     cmds = []
-    for src in SOURCES:
+    for src in sources:
         obj = os.path.join(obj_dir, os.path.splitext(src)[0] + ".o")
         objs.append(obj)
         lang = ["-x", "hip"] if src.endswith(".hip") else []
@@ -62,11 +64,20 @@ def build_library(out_dir: str = PKG, verbose: bool = False) -> str:
                      os.path.join(CSRC, src), "-o", obj])
     with ThreadPoolExecutor(max_workers=len(cmds)) as ex:
         list(ex.map(lambda c: _run(c, verbose), cmds))
-    out = os.path.join(out_dir, LIB_NAME)
+    out = os.path.join(out_dir, name)
     tmp = out + ".tmp"
     _run([hipcc, f"--offload-arch={ARCH}", "-shared", "-fPIC", *objs, "-o", tmp], verbose)
     os.replace(tmp, out)
     return out
+
+
+def build_library(out_dir: str = PKG, verbose: bool = False) -> str:
+    """Build the decode-attention library and the measurement probe library; return the former's path."""
+    with ThreadPoolExecutor(max_workers=2) as ex:
+        main = ex.submit(_build_one, LIB_NAME, SOURCES, out_dir, verbose)
+        probe = ex.submit(_build_one, PROBE_LIB_NAME, PROBE_SOURCES, out_dir, verbose)
+        probe.result()
+        return main.result()
 
 
 if __name__ == "__main__":

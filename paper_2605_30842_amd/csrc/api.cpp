@@ -12,8 +12,11 @@
 
 namespace comem {
 using KernelFn = void (*)(AttnParams);
+using QueueKernelFn = void (*)(AttnParams, int);
 KernelFn select_mfma_kernel(int head_dim, bool paged, int page_size);
+QueueKernelFn select_mfma_queue_kernel(int head_dim, bool paged, int page_size);
 int mfma_max_split_pages();
+int mfma_max_queue_batch();
 KernelFn select_valu_kernel(bool bf16, int head_dim, int group, bool paged);
 }  // namespace comem
 
@@ -22,6 +25,7 @@ namespace {
 constexpr uint64_t kPlanMagic = 0x434f4d454d444131ull;  // "COMEMDA1"
 constexpr int kAssumedCUs = 256;                        // gfx950 (MI355X) without a device query
 constexpr int64_t kTargetWgsPerCu = 2;                  // workgroups per compute unit for one full round
+constexpr int kQueueWgsPerCu = 2;                       // resident workgroups per compute unit (MFMA kernel)
 constexpr int64_t kMinChunk = 256;                      // tokens per split, lower bound
 constexpr int64_t kMaxChunk = 2048;                     // tokens per split, upper bound (auto plan)
 constexpr int64_t kMaxContext = int64_t{1} << 30;
@@ -46,6 +50,7 @@ struct comem_decode_attn_plan {
 namespace {
 
 int group_of(const comem_decode_attn_config& c) { return c.num_q_heads / c.num_kv_heads; }
+bool uses_mfma(const comem_decode_attn_plan& p);
 int elem_bytes(const comem_decode_attn_config& c) { return c.dtype == COMEM_F32 ? 4 : 2; }
 
 // Workspace bytes for `slots` (sequence, split) partial results: ticket
@@ -61,6 +66,18 @@ size_t call_workspace_bytes(const comem_decode_attn_plan& p, int64_t batch, int6
   return splits <= 1 ? 0 : slots_workspace_bytes(p, batch * splits);
 }
 
+// Tokens per split for the matrix-core kernel, from the host-side bounds of
+// a call (the device-side lengths are never read on the host). Splits of
+// 4096 tokens keep contexts of 128k and more at <= 32 splits; otherwise 2048
+// if that still leaves >= 8 work items per resident workgroup (so the work
+// queue can balance them), else 1024.
+int64_t mfma_chunk(const comem_decode_attn_plan& p, int64_t batch, int64_t L) {
+  if (L >= 32 * 4096) return 4096;
+  const int64_t resident = static_cast<int64_t>(kQueueWgsPerCu) * p.num_cus;
+  if (batch * p.cfg.num_kv_heads * ceil_div(L, 2048) >= 8 * resident) return 2048;
+  return 1024;
+}
+
 // Choose tokens per split and the split count for one call.
 comem_status plan_call(const comem_decode_attn_plan& p, int64_t batch, int64_t max_ctx,
                        size_t ws_bytes, int64_t* chunk_out, int64_t* splits_out) {
@@ -70,12 +87,14 @@ comem_status plan_call(const comem_decode_attn_plan& p, int64_t batch, int64_t m
     chunk = p.cfg.chunk_tokens;
     if (call_workspace_bytes(p, batch, ceil_div(L, chunk)) > ws_bytes) return COMEM_ERR_WORKSPACE_TOO_SMALL;
   } else {
-    const int64_t target = kTargetWgsPerCu * p.num_cus;
-    const int64_t per = ceil_div(batch * p.cfg.num_kv_heads * L, target);
-    chunk = kMinChunk;
-    while (chunk < per && chunk < kMaxChunk) chunk *= 2;
-    if (chunk < kMinChunk) chunk = kMinChunk;
-    if (chunk > kMaxChunk) chunk = kMaxChunk;
+    if (uses_mfma(p)) {
+      chunk = mfma_chunk(p, batch, L);
+    } else {
+      const int64_t target = kTargetWgsPerCu * p.num_cus;
+      const int64_t per = ceil_div(batch * p.cfg.num_kv_heads * L, target);
+      chunk = kMinChunk;
+      while (chunk < per && chunk < kMaxChunk) chunk *= 2;
+    }
     while (call_workspace_bytes(p, batch, ceil_div(L, chunk)) > ws_bytes) {
       if (chunk >= L) return COMEM_ERR_WORKSPACE_TOO_SMALL;
       chunk *= 2;
@@ -99,9 +118,11 @@ comem_status validate_config(const comem_decode_attn_config& c) {
   if (c.max_ctx_len <= 0 || c.max_ctx_len > kMaxContext) return COMEM_ERR_INVALID_SHAPE;
   if (c.chunk_tokens < 0 || c.chunk_tokens % 32 != 0 || c.chunk_tokens > kMaxContext)
     return COMEM_ERR_INVALID_SHAPE;
-  if (c.variant != COMEM_VARIANT_AUTO && c.variant != COMEM_VARIANT_VALU && c.variant != COMEM_VARIANT_MFMA)
+  if (c.variant != COMEM_VARIANT_AUTO && c.variant != COMEM_VARIANT_VALU && c.variant != COMEM_VARIANT_MFMA &&
+      c.variant != COMEM_VARIANT_MFMA_GRID)
     return COMEM_ERR_UNSUPPORTED;
-  if (c.variant == COMEM_VARIANT_MFMA && c.dtype != COMEM_BF16) return COMEM_ERR_UNSUPPORTED;
+  if ((c.variant == COMEM_VARIANT_MFMA || c.variant == COMEM_VARIANT_MFMA_GRID) && c.dtype != COMEM_BF16)
+    return COMEM_ERR_UNSUPPORTED;
   return COMEM_OK;
 }
 
@@ -131,12 +152,33 @@ comem_status validate_common(const comem_decode_attn_plan& p, const void* q, con
 }
 
 bool uses_mfma(const comem_decode_attn_plan& p) {
-  return p.cfg.variant == COMEM_VARIANT_MFMA || (p.cfg.variant == COMEM_VARIANT_AUTO && p.cfg.dtype == COMEM_BF16);
+  return p.cfg.variant == COMEM_VARIANT_MFMA || p.cfg.variant == COMEM_VARIANT_MFMA_GRID ||
+         (p.cfg.variant == COMEM_VARIANT_AUTO && p.cfg.dtype == COMEM_BF16);
+}
+
+// The work-queue form of the matrix-core kernel keeps two counters after the
+// tickets, so it needs a workspace (of at least the ticket region).
+bool uses_queue(const comem_decode_attn_plan& p, int64_t batch, const void* workspace, size_t ws_bytes) {
+  return uses_mfma(p) && p.cfg.variant != COMEM_VARIANT_MFMA_GRID && batch <= comem::mfma_max_queue_batch() &&
+         workspace != nullptr && ws_bytes >= p.ticket_bytes;
 }
 
 comem_status launch(const comem_decode_attn_plan& p, bool paged, comem::AttnParams& a, int64_t batch,
-                    int64_t splits, void* stream) {
+                    int64_t splits, bool queue, void* stream) {
   const bool bf16 = p.cfg.dtype == COMEM_BF16;
+  if (queue) {
+    comem::QueueKernelFn qfn = comem::select_mfma_queue_kernel(p.cfg.head_dim, paged, a.page_mask + 1);
+    if (qfn == nullptr) return COMEM_ERR_UNSUPPORTED;
+    const int64_t items = batch * p.cfg.num_kv_heads * splits;
+    const int64_t resident = static_cast<int64_t>(kQueueWgsPerCu) * p.num_cus;
+    dim3 grid(static_cast<unsigned>(items < resident ? items : resident));
+    dim3 block(comem::kThreads);
+    int nb = static_cast<int>(batch);
+    void* args[] = {&a, &nb};
+    const hipError_t err = hipLaunchKernel(reinterpret_cast<const void*>(qfn), grid, block, args, 0,
+                                           static_cast<hipStream_t>(stream));
+    return err == hipSuccess ? COMEM_OK : COMEM_ERR_HIP;
+  }
   comem::KernelFn fn = uses_mfma(p) ? comem::select_mfma_kernel(p.cfg.head_dim, paged, a.page_mask + 1)
                                     : comem::select_valu_kernel(bf16, p.cfg.head_dim, group_of(p.cfg), paged);
   if (fn == nullptr) return COMEM_ERR_UNSUPPORTED;
@@ -151,7 +193,8 @@ comem_status launch(const comem_decode_attn_plan& p, bool paged, comem::AttnPara
 
 void fill_common(const comem_decode_attn_plan& p, comem::AttnParams& a, const void* q, const void* k,
                  const void* v, int64_t stride_token, int64_t stride_head, const int32_t* ctx_lens,
-                 float* out, float* lse, void* workspace, int64_t batch, int64_t chunk, int64_t splits) {
+                 float* out, float* lse, void* workspace, int64_t batch, int64_t chunk, int64_t splits,
+                 bool queue) {
   const int64_t e = elem_bytes(p.cfg);
   std::memset(&a, 0, sizeof(a));
   a.q = static_cast<const char*>(q);
@@ -168,7 +211,8 @@ void fill_common(const comem_decode_attn_plan& p, comem::AttnParams& a, const vo
   a.chunk = static_cast<int32_t>(chunk);
   a.num_splits = static_cast<int32_t>(splits);
   a.scale_log2 = p.cfg.scale * 1.4426950408889634f;
-  if (splits > 1) {
+  a.queue_slot = p.cfg.max_batch * p.cfg.num_kv_heads;
+  if (splits > 1 || queue) {
     char* ws = static_cast<char*>(workspace);
     const size_t slots = static_cast<size_t>(batch) * static_cast<size_t>(splits) *
                          static_cast<size_t>(p.cfg.num_q_heads);
@@ -221,12 +265,17 @@ comem_status comem_decode_attn_init(const comem_decode_attn_config* cfg, int dev
   p->cfg = *cfg;
   p->device = device;
   p->num_cus = num_cus > 0 ? num_cus : kAssumedCUs;
-  p->ticket_bytes = align256(static_cast<size_t>(cfg->max_batch) * cfg->num_kv_heads * 4);
-  // Largest number of (sequence, split) slots any call within the limits plans.
+  // tickets (one per sequence and KV head), then the two work-queue counters
+  p->ticket_bytes = align256((static_cast<size_t>(cfg->max_batch) * cfg->num_kv_heads + 2) * 4);
+  // Largest number of (sequence, split) slots any call within the limits plans
+  // (bounded for the matrix-core kernel by its smallest split of 1024 tokens);
+  // calls with a smaller workspace get coarser splits.
   const int64_t B = cfg->max_batch, L = cfg->max_ctx_len;
   int64_t slots;
   if (cfg->chunk_tokens > 0) {
     slots = B * ceil_div(L, cfg->chunk_tokens);
+  } else if (uses_mfma(*p)) {
+    slots = B * ceil_div(L, 1024);
   } else {
     const int64_t target = kTargetWgsPerCu * p->num_cus;
     const int64_t a = ceil_div(target, cfg->num_kv_heads) + B;
@@ -281,10 +330,12 @@ comem_status comem_decode_attn(const comem_decode_attn_plan* plan, const void* q
   st = plan_call(*p, batch, max_ctx_len, workspace == nullptr ? 0 : workspace_bytes, &chunk, &splits);
   if (st != COMEM_OK) return st;
   if (p->device == COMEM_NO_DEVICE) return COMEM_ERR_NO_DEVICE;
+  const bool queue = uses_queue(*p, batch, workspace, workspace_bytes);
   comem::AttnParams a;
-  fill_common(*p, a, q, k, v, stride_token, stride_head, ctx_lens, out, lse, workspace, batch, chunk, splits);
+  fill_common(*p, a, q, k, v, stride_token, stride_head, ctx_lens, out, lse, workspace, batch, chunk, splits,
+              queue);
   a.seq_start = seq_start;
-  return launch(*p, false, a, batch, splits, hip_stream);
+  return launch(*p, false, a, batch, splits, queue, hip_stream);
 }
 
 comem_status comem_decode_attn_paged(const comem_decode_attn_plan* plan, const void* q,
@@ -312,9 +363,10 @@ comem_status comem_decode_attn_paged(const comem_decode_attn_plan* plan, const v
   // The matrix-core kernel stages one split's block-table entries in LDS.
   if (uses_mfma(*p) && (chunk - 1) / page_size + 2 > comem::mfma_max_split_pages()) return COMEM_ERR_INVALID_SHAPE;
   if (p->device == COMEM_NO_DEVICE) return COMEM_ERR_NO_DEVICE;
+  const bool queue = uses_queue(*p, batch, workspace, workspace_bytes);
   comem::AttnParams a;
   fill_common(*p, a, q, k_pages, v_pages, stride_token, stride_head, ctx_lens, out, lse, workspace, batch,
-              chunk, splits);
+              chunk, splits, queue);
   a.block_table = block_table;
   a.stride_page = stride_page * elem_bytes(p->cfg);
   a.max_pages = max_pages_per_seq;
@@ -322,7 +374,7 @@ comem_status comem_decode_attn_paged(const comem_decode_attn_plan* plan, const v
   while ((1 << shift) < page_size) ++shift;
   a.page_shift = shift;
   a.page_mask = page_size - 1;
-  return launch(*p, true, a, batch, splits, hip_stream);
+  return launch(*p, true, a, batch, splits, queue, hip_stream);
 }
 
 }  // extern "C"

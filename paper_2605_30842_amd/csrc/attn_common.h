@@ -49,7 +49,8 @@ struct AttnParams {
   int32_t chunk;       // tokens per split (multiple of 32)
   int32_t num_splits;  // gridDim.x
   float scale_log2;    // scale * log2(e)
-  uint32_t* tickets;   // [max_batch * Hkv], zero between calls
+  uint32_t* tickets;   // [max_batch * Hkv] tickets, then 2 queue counters; zero between calls
+  int32_t queue_slot;  // index of the queue counters in tickets
   float* lse_part;     // [B, Hkv, S, G]   (log2 units)
   float* o_part;       // [B, Hkv, S, G, D]
 };

@@ -41,12 +41,18 @@ typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
 template <int D>
 struct VRow;  // per-lane slice of one V row: NT bf16 values
+// V rows are read whole by consecutive lanes and never again: load them with
+// the non-temporal (streaming) cache policy. K rows are read in two halves
+// of a 128-byte line by consecutive instructions, so they keep the default
+// policy and the second half hits the line the first half brought in.
+constexpr int kStreaming = 2;
+
 template <>
 struct VRow<128> {
   u32x4 w;
   __device__ uint32_t word(int i) const { return w[i]; }
   __device__ void load(__amdgpu_buffer_rsrc_t r, uint32_t voff, int soff) {
-    w = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0));
+    w = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, kStreaming));
   }
 };
 template <>
@@ -54,7 +60,7 @@ struct VRow<64> {
   u32x2 w;
   __device__ uint32_t word(int i) const { return w[i]; }
   __device__ void load(__amdgpu_buffer_rsrc_t r, uint32_t voff, int soff) {
-    w = __builtin_bit_cast(u32x2, __builtin_amdgcn_raw_buffer_load_b64(r, voff, soff, 0));
+    w = __builtin_bit_cast(u32x2, __builtin_amdgcn_raw_buffer_load_b64(r, voff, soff, kStreaming));
   }
 };
 
@@ -70,6 +76,8 @@ __device__ inline bf16x8 as_bf16x8(u32x4 x) { return __builtin_bit_cast(bf16x8, 
 // Page lookups of one split go through LDS: the workgroup copies the split's
 // block-table entries there once, so the token loop never waits on them.
 constexpr int kMaxSplitPages = 2048;
+// Largest batch the work-queue kernel takes (its per-sequence split offsets live in LDS).
+constexpr int kMaxQueueBatch = 4096;
 
 enum class Layout { kContig, kPaged, kPagedFine };
 
@@ -101,8 +109,10 @@ struct Loader {
   // contiguous layout): per half, one buffer descriptor on the half's first
   // row (uniform, in SGPRs) and fixed 32-bit lane offsets. The descriptor's
   // size covers exactly the 16 rows, so the hardware returns zeros instead of
-  // touching memory should an offset ever fall outside them.
-  __device__ void load_full(Tile<D>& T, int t0) const {
+  // touching memory should an offset ever fall outside them. With `repeat`
+  // the call only keeps the load count of the pipeline steady: it re-reads
+  // the tile's K rows (still cached) into both halves and its data is unused.
+  __device__ void load_full(Tile<D>& T, int t0, bool repeat) const {
     constexpr int KB = D / 32;
     const int extent = static_cast<int>(15 * stride_token + 2 * D);
 #pragma unroll
@@ -110,8 +120,8 @@ struct Loader {
       const int64_t base = uniform_i64(token_offset(t0 + 16 * s));
       const __amdgpu_buffer_rsrc_t rk =
           __builtin_amdgcn_make_buffer_rsrc(const_cast<char*>(kbase + base), 0, extent, kBufferConfig);
-      const __amdgpu_buffer_rsrc_t rv =
-          __builtin_amdgcn_make_buffer_rsrc(const_cast<char*>(vbase + base), 0, extent, kBufferConfig);
+      const __amdgpu_buffer_rsrc_t rv = __builtin_amdgcn_make_buffer_rsrc(
+          const_cast<char*>((repeat ? kbase : vbase) + base), 0, extent, kBufferConfig);
 #pragma unroll
       for (int kk = 0; kk < KB; ++kk)
         T.k[s][kk] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rk, koff + 64 * kk, 0, 0));
@@ -213,23 +223,33 @@ __device__ inline void compute_tile(const Tile<D>& T, int t0, int t_end, int c, 
   }
 }
 
+// Shared memory of one workgroup; the page table and the wave states are
+// rewritten for every split the workgroup processes.
 template <int D, Layout LAYOUT>
-__global__ __launch_bounds__(kThreads, 2) void decode_mfma_kernel(const AttnParams p) {
+struct SplitSmem {
+  WaveState<D> ws;
+  int32_t pages[LAYOUT == Layout::kContig ? 1 : kMaxSplitPages];
+};
+
+// Attention of the G query heads of KV head hk of sequence b over split j
+// (tokens [j * chunk, min((j + 1) * chunk, L))), ending with this split's
+// share of the log-sum-exp merge. Called by every thread of the workgroup.
+//
+// With next_item set (work-queue form), thread 0 takes the workgroup's next
+// item from the queue once the token loop is done: issued earlier, the queue
+// atomic would sit ahead of the tile loads in the in-order memory counter.
+template <int D, Layout LAYOUT>
+__device__ void attend_split(const AttnParams& p, SplitSmem<D, LAYOUT>& sm, int b, int hk, int j, int L,
+                             int* next_item) {
   constexpr int KB = D / 32;
   constexpr int NT = D / 16;
-  const int j = blockIdx.x, hk = blockIdx.y, b = blockIdx.z;
-  const int L = p.ctx_lens[b];
   const int nsplit_b = L > 0 ? 1 + (L - 1) / p.chunk : 1;
-  if (j >= nsplit_b) return;
   const int t_begin = j * p.chunk;
   const int t_end = t_begin + min(L - t_begin, p.chunk);
   const int lane = threadIdx.x & 63;
   const int w = uniform_i32(threadIdx.x >> 6);
   const int c = lane & 15, g = lane >> 4;
   const int G = p.group;
-
-  __shared__ WaveState<D> ws;
-  __shared__ int32_t sm_pages[LAYOUT == Layout::kContig ? 1 : kMaxSplitPages];
 
   Loader<D, LAYOUT> ld;
   ld.kbase = p.k + hk * p.stride_head;
@@ -244,10 +264,10 @@ __global__ __launch_bounds__(kThreads, 2) void decode_mfma_kernel(const AttnPara
     const int first = t_begin >> p.page_shift;
     const int count = ((t_end - 1) >> p.page_shift) - first + 1;
     const int32_t* row = p.block_table + static_cast<int64_t>(b) * p.max_pages + first;
-    for (int i = threadIdx.x; i < count; i += kThreads) sm_pages[i] = row[i];
+    for (int i = threadIdx.x; i < count; i += kThreads) sm.pages[i] = row[i];
     __syncthreads();
   }
-  ld.sm_pages = sm_pages;
+  ld.sm_pages = sm.pages;
   ld.stride_token = p.stride_token;
   ld.stride_page = p.stride_page;
   ld.page_shift = p.page_shift;
@@ -282,20 +302,20 @@ __global__ __launch_bounds__(kThreads, 2) void decode_mfma_kernel(const AttnPara
   if constexpr (LAYOUT != Layout::kPagedFine) {
     // Full tiles w, w + 4, ...: while one tile is computed the next is in
     // flight. The prefetch is issued unconditionally (past the last full tile
-    // it re-reads the current one, which is still cached) and pinned ahead of
-    // the compute, so the compiler waits for exactly the older tile's loads.
+    // it re-reads cached K rows of the current one) and pinned ahead of the
+    // compute, so the compiler waits for exactly the older tile's loads.
     if (ti < nfull) {
       Tile<D> A, B;
-      ld.load_full(A, t_begin + 32 * ti);
+      ld.load_full(A, t_begin + 32 * ti, false);
       for (;;) {
         int nx = ti + kWaves;
-        ld.load_full(B, t_begin + 32 * (nx < nfull ? nx : ti));
+        ld.load_full(B, t_begin + 32 * (nx < nfull ? nx : ti), nx >= nfull);
         __builtin_amdgcn_sched_barrier(0);
         compute_tile<D>(A, t_begin + 32 * ti, t_end, c, g, qop, p.scale_log2, m_run, l_run, acc);
         if (nx >= nfull) break;
         ti = nx;
         nx = ti + kWaves;
-        ld.load_full(A, t_begin + 32 * (nx < nfull ? nx : ti));
+        ld.load_full(A, t_begin + 32 * (nx < nfull ? nx : ti), nx >= nfull);
         __builtin_amdgcn_sched_barrier(0);
         compute_tile<D>(B, t_begin + 32 * ti, t_end, c, g, qop, p.scale_log2, m_run, l_run, acc);
         if (nx >= nfull) break;
@@ -316,28 +336,109 @@ __global__ __launch_bounds__(kThreads, 2) void decode_mfma_kernel(const AttnPara
     }
   }
 
+  if (next_item != nullptr && threadIdx.x == 0)
+    *next_item = static_cast<int>(gridDim.x + atomicAdd(p.tickets + p.queue_slot, 1u));
+
   // Wave totals: l over the four lane groups; state to LDS.
   l_run += __shfl_xor(l_run, 16);
   l_run += __shfl_xor(l_run, 32);
   if (g == 0 && c < G) {
-    ws.m[w][c] = m_run;
-    ws.l[w][c] = l_run;
+    sm.ws.m[w][c] = m_run;
+    sm.ws.l[w][c] = l_run;
   }
 #pragma unroll
   for (int r = 0; r < 4; ++r) {
     const int h = 4 * g + r;
     if (h < G) {
 #pragma unroll
-      for (int n = 0; n < NT; ++n) ws.o[w][h][NT * c + n] = acc[n][r];
+      for (int n = 0; n < NT; ++n) sm.ws.o[w][h][NT * c + n] = acc[n][r];
     }
   }
   __syncthreads();
-  finalize_split<D>(p, ws, b, hk, j, nsplit_b);
+  finalize_split<D>(p, sm.ws, b, hk, j, nsplit_b);
+}
+
+// One workgroup per (split, KV head, sequence); splits past a sequence's end exit.
+template <int D, Layout LAYOUT>
+__global__ __launch_bounds__(kThreads, 2) void decode_mfma_kernel(const AttnParams p) {
+  const int j = blockIdx.x, hk = blockIdx.y, b = blockIdx.z;
+  const int L = p.ctx_lens[b];
+  const int nsplit_b = L > 0 ? 1 + (L - 1) / p.chunk : 1;
+  if (j >= nsplit_b) return;
+  __shared__ SplitSmem<D, LAYOUT> sm;
+  attend_split<D, LAYOUT>(p, sm, b, hk, j, L, nullptr);
+}
+
+// Persistent workgroups that take work items from a queue. Item i stands for
+// split j of KV head hk of sequence b, in the order (b, j, hk): the heads of
+// one token range are adjacent, sequences follow each other. Which workgroup
+// runs an item depends on timing, but every item computes the same values
+// and the merge order is fixed, so results do not. The queue counter and the
+// count of finished workgroups live next to the tickets and return to zero
+// when the last workgroup leaves. Faster XCDs and compute units simply take
+// more items, and ragged batches need no empty workgroups.
+template <int D, Layout LAYOUT>
+__global__ __launch_bounds__(kThreads, 2) void decode_mfma_queue_kernel(const AttnParams p, int batch) {
+  __shared__ SplitSmem<D, LAYOUT> sm;
+  __shared__ int sm_first[kMaxQueueBatch + 1];  // first split index of each sequence; last = total
+  __shared__ int sm_next;
+  const int tid = threadIdx.x;
+  uint32_t* queue = p.tickets + p.queue_slot;
+  uint32_t* finished = queue + 1;
+
+  // Splits per sequence, then an exclusive prefix sum (one wave scans).
+  for (int b = tid; b < batch; b += kThreads) {
+    const int L = p.ctx_lens[b];
+    sm_first[b + 1] = L > 0 ? 1 + (L - 1) / p.chunk : 1;
+  }
+  __syncthreads();
+  if (tid < 64) {
+    int carry = 0;
+    for (int base = 0; base < batch; base += 64) {
+      const int i = base + tid;
+      int v = i < batch ? sm_first[i + 1] : 0;
+#pragma unroll
+      for (int o = 1; o < 64; o <<= 1) {
+        const int u = __shfl_up(v, o);
+        if (tid >= o) v += u;
+      }
+      if (i < batch) sm_first[i + 1] = carry + v;
+      carry += __shfl(v, 63);
+    }
+    if (tid == 0) sm_first[0] = 0;
+  }
+  __syncthreads();
+  const int total = sm_first[batch] * p.num_kv_heads;
+  // Item blockIdx.x first; later items come from the queue, which hands out
+  // gridDim.x, gridDim.x + 1, ... Without more items than workgroups the
+  // queue is never touched.
+  const bool queued = total > static_cast<int>(gridDim.x);
+
+  int item = blockIdx.x;
+  while (item < total) {
+    const int split_index = item / p.num_kv_heads;
+    const int hk = item - split_index * p.num_kv_heads;
+    int lo = 0, hi = batch - 1;  // sequence b with sm_first[b] <= split_index < sm_first[b + 1]
+    while (lo < hi) {
+      const int mid = (lo + hi + 1) >> 1;
+      if (sm_first[mid] <= split_index) lo = mid; else hi = mid - 1;
+    }
+    const int b = lo;
+    attend_split<D, LAYOUT>(p, sm, b, hk, split_index - sm_first[b], p.ctx_lens[b], queued ? &sm_next : nullptr);
+    __syncthreads();
+    item = queued ? sm_next : total;
+    __syncthreads();
+  }
+  if (queued && tid == 0 && atomicAdd(finished, 1u) == gridDim.x - 1) {
+    atomicExch(queue, 0u);
+    atomicExch(finished, 0u);
+  }
 }
 
 }  // namespace
 
 using KernelFn = void (*)(AttnParams);
+using QueueKernelFn = void (*)(AttnParams, int);
 
 template <int D>
 KernelFn pick_layout(bool paged, int page_size) {
@@ -345,11 +446,26 @@ KernelFn pick_layout(bool paged, int page_size) {
   return page_size >= 16 ? decode_mfma_kernel<D, Layout::kPaged> : decode_mfma_kernel<D, Layout::kPagedFine>;
 }
 
+template <int D>
+QueueKernelFn pick_queue_layout(bool paged, int page_size) {
+  if (!paged) return decode_mfma_queue_kernel<D, Layout::kContig>;
+  return page_size >= 16 ? decode_mfma_queue_kernel<D, Layout::kPaged>
+                         : decode_mfma_queue_kernel<D, Layout::kPagedFine>;
+}
+
 KernelFn select_mfma_kernel(int head_dim, bool paged, int page_size) {
   if (head_dim == 128) return pick_layout<128>(paged, page_size);
   if (head_dim == 64) return pick_layout<64>(paged, page_size);
   return nullptr;
 }
+
+QueueKernelFn select_mfma_queue_kernel(int head_dim, bool paged, int page_size) {
+  if (head_dim == 128) return pick_queue_layout<128>(paged, page_size);
+  if (head_dim == 64) return pick_queue_layout<64>(paged, page_size);
+  return nullptr;
+}
+
+int mfma_max_queue_batch() { return kMaxQueueBatch; }
 
 int mfma_max_split_pages() { return kMaxSplitPages; }
 

@@ -35,6 +35,15 @@ def test_library_exports_every_declared_symbol():
         assert hasattr(lib, name), name
 
 
+def test_probe_library_exports_its_header():
+    text = re.sub(r"/\*.*?\*/", "", open(os.path.join(ROOT, "include", "comem_probe.h")).read(), flags=re.S)
+    names = sorted(set(re.findall(r"\b(comem_[a-z_]+)\s*\(", text)))
+    assert names == sorted(B.PROBE_EXPORTED)
+    lib = B.load_probe_library()
+    for name in names:
+        assert hasattr(lib, name), name
+
+
 def _cfg(**kw):
     base = dict(num_q_heads=32, num_kv_heads=8, head_dim=128, dtype=B.BF16, scale=0.088, max_batch=4,
                 max_ctx_len=4096, chunk_tokens=0, variant=B.VARIANT_AUTO)

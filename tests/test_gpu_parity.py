@@ -52,7 +52,7 @@ def test_fp32_ragged(chunk):
     check(out, lse, ro, rl, "f32", f"fp32 ragged chunk={chunk}")
 
 
-@pytest.mark.parametrize("variant", ["mfma", "valu"])
+@pytest.mark.parametrize("variant", ["mfma", "mfma_grid", "valu"])
 @pytest.mark.parametrize("chunk", [0, 32, 96, 256, 2048])
 def test_bf16_ragged_contiguous(variant, chunk):
     spec = small_spec(WORKLOADS[2], RAGGED, seed=22)
@@ -60,7 +60,7 @@ def test_bf16_ragged_contiguous(variant, chunk):
     check(out, lse, ro, rl, "bf16", f"bf16 ragged {variant} chunk={chunk}")
 
 
-@pytest.mark.parametrize("variant", ["mfma", "valu"])
+@pytest.mark.parametrize("variant", ["mfma", "mfma_grid", "valu"])
 @pytest.mark.parametrize("G", [1, 2, 4, 8, 16])
 @pytest.mark.parametrize("D", [64, 128])
 def test_groups_and_head_dims(variant, G, D):
@@ -77,7 +77,7 @@ def test_fp32_groups(G, D):
     check(out, lse, ro, rl, "f32", f"fp32 G={G} D={D}")
 
 
-@pytest.mark.parametrize("variant", ["mfma", "valu"])
+@pytest.mark.parametrize("variant", ["mfma", "mfma_grid", "valu"])
 @pytest.mark.parametrize("ps", [1, 8, 16, 64, 128])
 def test_paged_small(variant, ps):
     spec = small_spec(WORKLOADS[4], RAGGED, seed=25 + ps, max_ctx_len=4224).replace(page_size=ps)
@@ -85,7 +85,7 @@ def test_paged_small(variant, ps):
     check(out, lse, ro, rl, "bf16", f"paged ps={ps} {variant}")
 
 
-@pytest.mark.parametrize("variant", ["mfma", "valu"])
+@pytest.mark.parametrize("variant", ["mfma", "mfma_grid", "valu"])
 def test_empty_and_one_token(variant):
     spec = small_spec(WORKLOADS[2], [0, 1, 0, 1, 2], seed=26)
     w, _, _, out, lse, ro, rl = _case(spec, variant=variant)
@@ -97,7 +97,7 @@ def test_empty_and_one_token(variant):
     check(out, lse, ro, rl, "bf16", f"empty/one {variant}")
 
 
-@pytest.mark.parametrize("variant", ["mfma", "valu"])
+@pytest.mark.parametrize("variant", ["mfma", "mfma_grid", "valu"])
 def test_zero_query_gives_mean_of_structured_values(variant):
     """q = 0: every weight equal, out = mean of V. V[t] = (t mod 97) / 32 is exact in bf16."""
     from workloads.synth import f32_to_bf16_bits
@@ -116,7 +116,7 @@ def test_zero_query_gives_mean_of_structured_values(variant):
     assert np.abs(lse - np.log(L)).max() <= 1e-5
 
 
-@pytest.mark.parametrize("variant", ["mfma", "valu"])
+@pytest.mark.parametrize("variant", ["mfma", "mfma_grid", "valu"])
 def test_nan_poison_outside_contexts(variant):
     spec = small_spec(WORKLOADS[2], [5, 33, 0, 300], seed=28)
     _, _, _, out, lse, ro, rl = _case(spec, variant=variant, chunk=64, gap_rows=40, poison=True)
@@ -126,7 +126,7 @@ def test_nan_poison_outside_contexts(variant):
     check(out, lse, ro, rl, "bf16", f"poison paged {variant}")
 
 
-@pytest.mark.parametrize("variant", ["mfma", "valu"])
+@pytest.mark.parametrize("variant", ["mfma", "mfma_grid", "valu"])
 @pytest.mark.parametrize("ps", [16, 64])
 def test_paged_equals_contiguous_bitwise(variant, ps):
     """Same logical rows, same split plan: the paged and packed calls agree bit for bit."""
@@ -151,7 +151,7 @@ def test_paged_equals_contiguous_bitwise(variant, ps):
     torch.cuda.synchronize()
 
 
-@pytest.mark.parametrize("variant", ["mfma", "valu"])
+@pytest.mark.parametrize("variant", ["mfma", "mfma_grid", "valu"])
 def test_bitwise_reproducible(variant):
     spec = small_spec(WORKLOADS[2], [4096, 3000, 77], seed=31)
     w = generate(spec)
@@ -164,7 +164,7 @@ def test_bitwise_reproducible(variant):
         assert np.array_equal(first[0], again[0]) and np.array_equal(first[1], again[1])
 
 
-@pytest.mark.parametrize("variant", ["mfma", "valu"])
+@pytest.mark.parametrize("variant", ["mfma", "mfma_grid", "valu"])
 def test_fused_kv_buffer_strides(variant):
     """K and V interleaved in one [T, 2, Hkv, D] buffer: stride_token = 2 * Hkv * D."""
     import torch
@@ -206,7 +206,7 @@ def test_lse_optional():
     check(out, None, *da.reference(w), "bf16", "no lse")
 
 
-@pytest.mark.parametrize("variant", ["mfma", "valu"])
+@pytest.mark.parametrize("variant", ["mfma", "mfma_grid", "valu"])
 def test_split_merge_stress(variant):
     """Up to 256 splits per (sequence, KV head) and 16k workgroups: every split's
     partial result must reach the merging workgroup, call after call."""
