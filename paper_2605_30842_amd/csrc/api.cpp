@@ -166,11 +166,13 @@ bool uses_queue(const comem_decode_attn_plan& p, int64_t batch, const void* work
 comem_status launch(const comem_decode_attn_plan& p, bool paged, comem::AttnParams& a, int64_t batch,
                     int64_t splits, bool queue, void* stream) {
   const bool bf16 = p.cfg.dtype == COMEM_BF16;
-  if (queue) {
+  const int64_t items = batch * p.cfg.num_kv_heads * splits;
+  const int64_t resident = static_cast<int64_t>(kQueueWgsPerCu) * p.num_cus;
+  // With no more (nominal) items than resident workgroups every item gets its
+  // own workgroup anyway, and the grid form saves the queue's prologue.
+  if (queue && items > resident) {
     comem::QueueKernelFn qfn = comem::select_mfma_queue_kernel(p.cfg.head_dim, paged, a.page_mask + 1);
     if (qfn == nullptr) return COMEM_ERR_UNSUPPORTED;
-    const int64_t items = batch * p.cfg.num_kv_heads * splits;
-    const int64_t resident = static_cast<int64_t>(kQueueWgsPerCu) * p.num_cus;
     dim3 grid(static_cast<unsigned>(items < resident ? items : resident));
     dim3 block(comem::kThreads);
     int nb = static_cast<int>(batch);

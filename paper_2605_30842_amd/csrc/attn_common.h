@@ -25,6 +25,7 @@ typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 constexpr int kWaves = 4;           // waves per workgroup
 constexpr int kThreads = 64 * kWaves;
 constexpr int kMaxGroup = 16;       // largest GQA group handled in one workgroup
+constexpr int kMergeBatch = 16;     // split partials loaded together by one thread in the merge
 constexpr float kLn2 = 0.69314718055994530942f;
 
 // Kernel arguments (passed by value). Offsets and strides are in bytes.
@@ -203,19 +204,20 @@ __device__ void finalize_split(const AttnParams& p, const WaveState<D>& ws, int 
     const int h = (slot * 4) / D;
     const int d0 = slot * 4 - h * D;
     MergeState st;
-    // Batches of 8 splits: all 16 loads of a batch are in flight together.
-    // Indices past the last split re-read the last one and get weight 0.
-    for (int s0 = sub; s0 < nsplit_b; s0 += 8 * tps) {
-      float l2[8];
-      float4 o[8];
+    // Batches of kMergeBatch splits: all loads of a batch are in flight
+    // together. Indices past the last split re-read the last one and get
+    // weight 0.
+    for (int s0 = sub; s0 < nsplit_b; s0 += kMergeBatch * tps) {
+      float l2[kMergeBatch];
+      float4 o[kMergeBatch];
 #pragma unroll
-      for (int i = 0; i < 8; ++i) {
+      for (int i = 0; i < kMergeBatch; ++i) {
         const int si = min(s0 + i * tps, nsplit_b - 1);
         l2[i] = load_coherent(rl, (si * G + h) * 4);
         o[i] = load4_coherent(ro, ((si * G + h) * D + d0) * 4);
       }
 #pragma unroll
-      for (int i = 0; i < 8; ++i) st.add(s0 + i * tps < nsplit_b ? l2[i] : -INFINITY, 1.f, o[i]);
+      for (int i = 0; i < kMergeBatch; ++i) st.add(s0 + i * tps < nsplit_b ? l2[i] : -INFINITY, 1.f, o[i]);
     }
     if (tps == 1) {
       const float inv = 1.f / st.wsum;
