@@ -45,6 +45,9 @@ def _args():
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--workload", type=int, default=2, help="named workload 1..5 (2 = the headline one)")
+    ap.add_argument("--op", default="attention", choices=["attention", "append", "step"],
+                    help="attention: the decode-attention call; append: the KV-append call alone; "
+                         "step: append then attention, as one decode step runs them")
     ap.add_argument("--variant", default="auto", choices=["auto", "mfma", "mfma_grid", "valu"])
     ap.add_argument("--chunk", type=int, default=0, help="tokens per split (0 = planned)")
     ap.add_argument("--copies", type=int, default=0, help="KV copies to cycle over (0 = enough to exceed the LLC)")
@@ -120,7 +123,7 @@ def summarize(a):
       DIR/pmc/w<N>_fetch, DIR/pmc/w<N>_write   FETCH_SIZE / WRITE_SIZE runs of workload N
       DIR/pmc/copy_fetch, DIR/pmc/copy_write   the same counters on a 256 MiB copy
     """
-    from workloads.synth import WORKLOADS, generate
+    from workloads.synth import WORKLOADS, draw_new_rows, generate
 
     d = a.summarize
     cal_f = _counter_medians(os.path.join(d, "pmc", "copy_fetch")).get(("copy", "FETCH_SIZE"))
@@ -267,7 +270,7 @@ def main():
 
     from paper_2605_30842_amd import binding
     from paper_2605_30842_amd.binding import DecodeAttention
-    from workloads.synth import WORKLOADS, generate
+    from workloads.synth import WORKLOADS, draw_new_rows, generate
 
     binding.load_library()
     spec = WORKLOADS[a.workload]
@@ -294,14 +297,23 @@ def main():
     op = DecodeAttention(spec.num_q_heads, spec.num_kv_heads, spec.head_dim, spec.dtype, float(spec.scale),
                          spec.batch, spec.max_ctx_len, chunk_tokens=a.chunk, variant=a.variant)
     chunk, splits = op.splits(spec.batch, spec.max_ctx_len)
-    out = torch.empty((spec.batch, spec.num_q_heads, spec.head_dim), dtype=torch.float32, device=dev)
+    out = torch.zeros((spec.batch, spec.num_q_heads, spec.head_dim), dtype=torch.float32, device=dev)
     lse = torch.empty((spec.batch, spec.num_q_heads), dtype=torch.float32, device=dev)
+    new_k, new_v = (dev_t(x) for x in draw_new_rows(spec, seed=spec.seed + 100))
+    attend = a.op != "append"
+
     def step(i, stream):
         k, v = kv[i % copies]
-        if paged:
-            op.forward_paged(q, k, v, bt, ctx, spec.max_ctx_len, out=out, lse=lse, stream=stream)
-        else:
-            op.forward(q, k, v, ss, ctx, spec.max_ctx_len, out=out, lse=lse, stream=stream)
+        if a.op != "attention":  # the new token's rows are stored first (same row on every step)
+            if paged:
+                op.append_paged(new_k, new_v, k, v, bt, ctx, spec.max_ctx_len, stream=stream)
+            else:
+                op.append(new_k, new_v, k, v, ss, ctx, spec.max_ctx_len, stream=stream)
+        if attend:
+            if paged:
+                op.forward_paged(q, k, v, bt, ctx, spec.max_ctx_len, out=out, lse=lse, stream=stream)
+            else:
+                op.forward(q, k, v, ss, ctx, spec.max_ctx_len, out=out, lse=lse, stream=stream)
 
     stream = torch.cuda.current_stream()
     for i in range(a.warmup):
@@ -339,10 +351,26 @@ def main():
         replays = max(1, -(-a.steps // copies))
         steps = replays * copies
         ms = timed(lambda: [graph.replay() for _ in range(replays)], steps)
+    if a.op == "append":
+        row_bytes = spec.batch * spec.num_kv_heads * spec.head_dim * spec.elem_bytes * 2  # K and V rows
+        moved = 2 * row_bytes  # each row read once and written once
+        gbps = moved / (ms * 1e-3) / 1e9
+        print(json.dumps({
+            "metric": "kv-append µs/step", "value": round(ms * 1e3, 3), "unit": "µs", "n_gpus": 1,
+            "steps": steps, "warmup": a.warmup, "ms_per_step": round(ms, 6), "higher_is_better": False,
+            "scaling": "weak", "vs_baseline": None, "dtype": spec.dtype, "data": "synthetic",
+            "config": {"workload": spec.name, "op": "append", "batch": spec.batch, "layout": spec.layout,
+                       "page_size": spec.page_size, "row_bytes_per_step": row_bytes, "timing": a.timing,
+                       "eager_us_per_step": round(eager_ms * 1e3, 3)},
+            "roofline": {"bound": "hbm", "achieved": round(gbps, 3), "peak": PEAK_HBM_GBPS, "unit": "GB/s",
+                         "frac": round(gbps / PEAK_HBM_GBPS, 6), "traffic": None},
+            "cpu_baseline": None,
+        }), flush=True)
+        return
     gbps = kv_bytes / (ms * 1e-3) / 1e9
     assert torch.isfinite(out).all().item()
 
-    cpu = _cpu_baseline(w, a.cpu_seconds) if a.cpu_seconds > 0 else None
+    cpu = _cpu_baseline(w, a.cpu_seconds) if a.cpu_seconds > 0 and a.op == "attention" else None
     kind = a.variant if a.variant != "auto" else ("mfma" if spec.dtype == "bf16" else "valu")
     line = {
         "metric": METRIC,
@@ -365,11 +393,12 @@ def main():
             "num_kv_heads": spec.num_kv_heads, "head_dim": spec.head_dim, "ctx_len_total": int(w.ctx_lens.sum()),
             "layout": spec.layout, "page_size": spec.page_size, "kv_bytes_per_step": kv_bytes,
             "kv_copies_cycled": copies, "chunk_tokens": chunk, "splits": splits, "kernel": kind,
-            "timing": a.timing, "eager_us_per_step": round(eager_ms * 1e3, 3),
+            "timing": a.timing, "eager_us_per_step": round(eager_ms * 1e3, 3), "op": a.op,
         },
         "roofline": {
             "bound": "hbm", "achieved": round(gbps, 2), "peak": PEAK_HBM_GBPS, "unit": "GB/s",
-            "frac": round(gbps / PEAK_HBM_GBPS, 4), "traffic": recorded_traffic(spec.name),
+            "frac": round(gbps / PEAK_HBM_GBPS, 4),
+            "traffic": recorded_traffic(spec.name) if a.op == "attention" else None,
         },
         "cpu_baseline": cpu,
     }

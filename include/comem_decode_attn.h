@@ -158,6 +158,35 @@ comem_status comem_decode_attn_paged(const comem_decode_attn_plan* plan, const v
                                      int32_t batch, int64_t max_ctx_len, float* out, float* lse,
                                      void* workspace, size_t workspace_bytes, void* hip_stream);
 
+/* KV append (paper Sec. 2.2): before the new query token attends, its key
+ * and value are concatenated to the caches. With ctx_lens[b] = L_b counting
+ * the new token, these calls store new_k[b] and new_v[b] as token L_b - 1 of
+ * sequence b, in the layout the matching attention call reads; every other
+ * cache element is left as it was. Run on the same stream before the
+ * attention call, it gives the append-then-attend order of a decode step.
+ * The rows are copied, so the stored bits equal the given ones.
+ *   new_k, new_v device [batch, h_kv, d_h] dense, dtype of the plan, 16-byte aligned.
+ *   k, v          the cache (written), addressed as in comem_decode_attn.
+ *   max_ctx_len   host bound, <= plan max_ctx_len.
+ * A sequence whose ctx_lens[b] is outside [1, max_ctx_len] (or, paged,
+ * whose block-table entry for token L_b - 1 lies outside [0, num_pages)) is
+ * skipped on the device; no error is reported for it. Other errors as for
+ * the attention calls; the plan's variant and workspace play no part. */
+comem_status comem_kv_append(const comem_decode_attn_plan* plan, const void* new_k, const void* new_v,
+                             void* k, void* v, int64_t stride_token, int64_t stride_head,
+                             const int64_t* seq_start, const int32_t* ctx_lens, int32_t batch,
+                             int64_t max_ctx_len, void* hip_stream);
+
+/* Paged form: token L_b - 1 goes to slot (L_b - 1) % page_size of page
+ * block_table[b * max_pages_per_seq + (L_b - 1) / page_size]; pages, strides
+ * and block table as in comem_decode_attn_paged. */
+comem_status comem_kv_append_paged(const comem_decode_attn_plan* plan, const void* new_k,
+                                   const void* new_v, void* k_pages, void* v_pages, int64_t stride_page,
+                                   int64_t stride_token, int64_t stride_head, int32_t page_size,
+                                   int64_t num_pages, const int32_t* block_table,
+                                   int32_t max_pages_per_seq, const int32_t* ctx_lens, int32_t batch,
+                                   int64_t max_ctx_len, void* hip_stream);
+
 #ifdef __cplusplus
 }
 #endif

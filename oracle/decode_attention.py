@@ -126,6 +126,43 @@ def paged_context(kv_pages: np.ndarray, block_table: np.ndarray, ctx_lens: np.nd
     return np.concatenate(rows, axis=0)
 
 
+# ---------------------------------------------------------------- KV append
+
+
+def append_contiguous(kv: np.ndarray, seq_start: np.ndarray, ctx_lens: np.ndarray,
+                      new_rows: np.ndarray) -> np.ndarray:
+    """Copy of a packed [T, Hkv, D] cache with each sequence's new token stored.
+
+    The decode step of Sec. 2.2 concatenates the new token's key (value) to
+    the cache before attending: with ctx_lens counting that token, its row is
+    seq_start[b] + ctx_lens[b] - 1. new_rows is [B, Hkv, D]; sequences with
+    ctx_lens[b] == 0 have no token to store.
+    """
+    out = np.array(kv, copy=True)
+    for b in range(len(ctx_lens)):
+        if int(ctx_lens[b]) > 0:
+            out[int(seq_start[b]) + int(ctx_lens[b]) - 1] = new_rows[b]
+    return out
+
+
+def append_paged(kv_pages: np.ndarray, block_table: np.ndarray, ctx_lens: np.ndarray,
+                 new_rows: np.ndarray) -> np.ndarray:
+    """Copy of a paged [P, page, Hkv, D] cache with each sequence's new token stored.
+
+    Token t = ctx_lens[b] - 1 of sequence b goes to page block_table[b, t // page] at slot t % page.
+    """
+    page_size = kv_pages.shape[1]
+    out = np.array(kv_pages, copy=True)
+    for b in range(len(ctx_lens)):
+        t = int(ctx_lens[b]) - 1
+        if t >= 0:
+            page = int(block_table[b, t // page_size])
+            if not 0 <= page < kv_pages.shape[0]:
+                raise IndexError(f"block_table[{b}, {t // page_size}] = {page} outside the pool")
+            out[page, t % page_size] = new_rows[b]
+    return out
+
+
 # ---------------------------------------------------------------- whole batch
 
 

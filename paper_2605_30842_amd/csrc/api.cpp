@@ -9,6 +9,7 @@
 
 #include "attn_common.h"
 #include "comem_decode_attn.h"
+#include "kv_append.h"
 
 namespace comem {
 using KernelFn = void (*)(AttnParams);
@@ -130,6 +131,26 @@ const comem_decode_attn_plan* checked(const comem_decode_attn_plan* p) {
   return (p != nullptr && p->magic == kPlanMagic) ? p : nullptr;
 }
 
+// Checks of the paged-layout arguments shared by attention and append.
+comem_status validate_paged(const comem_decode_attn_plan& p, int64_t stride_page, int32_t page_size,
+                            int64_t num_pages, const int32_t* block_table, int32_t max_pages_per_seq,
+                            int64_t max_ctx_len) {
+  if (block_table == nullptr) return COMEM_ERR_NULL_POINTER;
+  if (page_size <= 0 || page_size > 4096 || (page_size & (page_size - 1)) != 0) return COMEM_ERR_INVALID_SHAPE;
+  if (num_pages <= 0 || stride_page <= 0) return COMEM_ERR_INVALID_SHAPE;
+  if (max_pages_per_seq <= 0 || max_pages_per_seq < ceil_div(max_ctx_len, page_size))
+    return COMEM_ERR_INVALID_SHAPE;
+  if ((stride_page * elem_bytes(p.cfg)) % 16 != 0) return COMEM_ERR_MISALIGNED;
+  if (!aligned(block_table, 4)) return COMEM_ERR_MISALIGNED;
+  return COMEM_OK;
+}
+
+int log2_of(int32_t pow2) {
+  int shift = 0;
+  while ((1 << shift) < pow2) ++shift;
+  return shift;
+}
+
 // Checks shared by both compute calls.
 comem_status validate_common(const comem_decode_attn_plan& p, const void* q, const void* k, const void* v,
                              int64_t stride_token, int64_t stride_head, const int32_t* ctx_lens,
@@ -189,6 +210,44 @@ comem_status launch(const comem_decode_attn_plan& p, bool paged, comem::AttnPara
   dim3 block(comem::kThreads);
   void* args[] = {&a};
   const hipError_t err = hipLaunchKernel(reinterpret_cast<const void*>(fn), grid, block, args, 0,
+                                         static_cast<hipStream_t>(stream));
+  return err == hipSuccess ? COMEM_OK : COMEM_ERR_HIP;
+}
+
+// Checks of an append call; fills the kernel arguments shared by both layouts.
+comem_status prepare_append(const comem_decode_attn_plan& p, const void* new_k, const void* new_v, void* k,
+                            void* v, int64_t stride_token, int64_t stride_head, const int32_t* ctx_lens,
+                            int32_t batch, int64_t max_ctx_len, comem::AppendParams& a) {
+  if (batch < 0 || batch > p.cfg.max_batch) return COMEM_ERR_INVALID_SHAPE;
+  if (max_ctx_len < 0 || max_ctx_len > p.cfg.max_ctx_len) return COMEM_ERR_INVALID_SHAPE;
+  if (batch == 0) return COMEM_OK;
+  if (new_k == nullptr || new_v == nullptr || k == nullptr || v == nullptr || ctx_lens == nullptr)
+    return COMEM_ERR_NULL_POINTER;
+  if (stride_token <= 0 || stride_head < 0) return COMEM_ERR_INVALID_SHAPE;
+  if (p.cfg.num_kv_heads > 1 && stride_head == 0) return COMEM_ERR_INVALID_SHAPE;
+  const int64_t e = elem_bytes(p.cfg);
+  if ((stride_token * e) % 16 != 0 || (stride_head * e) % 16 != 0) return COMEM_ERR_MISALIGNED;
+  if (!aligned(new_k, 16) || !aligned(new_v, 16) || !aligned(k, 16) || !aligned(v, 16))
+    return COMEM_ERR_MISALIGNED;
+  std::memset(&a, 0, sizeof(a));
+  a.new_k = static_cast<const char*>(new_k);
+  a.new_v = static_cast<const char*>(new_v);
+  a.k = static_cast<char*>(k);
+  a.v = static_cast<char*>(v);
+  a.ctx_lens = ctx_lens;
+  a.stride_token = stride_token * e;
+  a.stride_head = stride_head * e;
+  a.max_ctx_len = max_ctx_len;
+  a.num_kv_heads = p.cfg.num_kv_heads;
+  a.chunks_per_head = static_cast<int32_t>(p.cfg.head_dim * e / 16);
+  return COMEM_OK;
+}
+
+comem_status launch_append(const comem::AppendParams& a, bool paged, int32_t batch, void* stream) {
+  comem::AppendParams args = a;
+  void* argv[] = {&args};
+  const hipError_t err = hipLaunchKernel(reinterpret_cast<const void*>(comem::select_append_kernel(paged)),
+                                         dim3(static_cast<unsigned>(batch)), dim3(comem::kThreads), argv, 0,
                                          static_cast<hipStream_t>(stream));
   return err == hipSuccess ? COMEM_OK : COMEM_ERR_HIP;
 }
@@ -352,13 +411,8 @@ comem_status comem_decode_attn_paged(const comem_decode_attn_plan* plan, const v
   comem_status st = validate_common(*p, q, k_pages, v_pages, stride_token, stride_head, ctx_lens, batch,
                                     max_ctx_len, out, lse, workspace);
   if (st != COMEM_OK || batch == 0) return st;
-  if (block_table == nullptr) return COMEM_ERR_NULL_POINTER;
-  if (page_size <= 0 || page_size > 4096 || (page_size & (page_size - 1)) != 0) return COMEM_ERR_INVALID_SHAPE;
-  if (num_pages <= 0 || stride_page <= 0) return COMEM_ERR_INVALID_SHAPE;
-  if (max_pages_per_seq <= 0 || max_pages_per_seq < ceil_div(max_ctx_len, page_size))
-    return COMEM_ERR_INVALID_SHAPE;
-  if ((stride_page * elem_bytes(p->cfg)) % 16 != 0) return COMEM_ERR_MISALIGNED;
-  if (!aligned(block_table, 4)) return COMEM_ERR_MISALIGNED;
+  st = validate_paged(*p, stride_page, page_size, num_pages, block_table, max_pages_per_seq, max_ctx_len);
+  if (st != COMEM_OK) return st;
   int64_t chunk = 0, splits = 0;
   st = plan_call(*p, batch, max_ctx_len, workspace == nullptr ? 0 : workspace_bytes, &chunk, &splits);
   if (st != COMEM_OK) return st;
@@ -372,11 +426,50 @@ comem_status comem_decode_attn_paged(const comem_decode_attn_plan* plan, const v
   a.block_table = block_table;
   a.stride_page = stride_page * elem_bytes(p->cfg);
   a.max_pages = max_pages_per_seq;
-  int shift = 0;
-  while ((1 << shift) < page_size) ++shift;
-  a.page_shift = shift;
+  a.page_shift = log2_of(page_size);
   a.page_mask = page_size - 1;
   return launch(*p, true, a, batch, splits, queue, hip_stream);
+}
+
+comem_status comem_kv_append(const comem_decode_attn_plan* plan, const void* new_k, const void* new_v,
+                             void* k, void* v, int64_t stride_token, int64_t stride_head,
+                             const int64_t* seq_start, const int32_t* ctx_lens, int32_t batch,
+                             int64_t max_ctx_len, void* hip_stream) {
+  const comem_decode_attn_plan* p = checked(plan);
+  if (p == nullptr) return COMEM_ERR_BAD_HANDLE;
+  comem::AppendParams a;
+  comem_status st = prepare_append(*p, new_k, new_v, k, v, stride_token, stride_head, ctx_lens, batch,
+                                   max_ctx_len, a);
+  if (st != COMEM_OK || batch == 0) return st;
+  if (seq_start == nullptr) return COMEM_ERR_NULL_POINTER;
+  if (!aligned(seq_start, 8)) return COMEM_ERR_MISALIGNED;
+  if (p->device == COMEM_NO_DEVICE) return COMEM_ERR_NO_DEVICE;
+  a.seq_start = seq_start;
+  return launch_append(a, false, batch, hip_stream);
+}
+
+comem_status comem_kv_append_paged(const comem_decode_attn_plan* plan, const void* new_k,
+                                   const void* new_v, void* k_pages, void* v_pages, int64_t stride_page,
+                                   int64_t stride_token, int64_t stride_head, int32_t page_size,
+                                   int64_t num_pages, const int32_t* block_table,
+                                   int32_t max_pages_per_seq, const int32_t* ctx_lens, int32_t batch,
+                                   int64_t max_ctx_len, void* hip_stream) {
+  const comem_decode_attn_plan* p = checked(plan);
+  if (p == nullptr) return COMEM_ERR_BAD_HANDLE;
+  comem::AppendParams a;
+  comem_status st = prepare_append(*p, new_k, new_v, k_pages, v_pages, stride_token, stride_head, ctx_lens,
+                                   batch, max_ctx_len, a);
+  if (st != COMEM_OK || batch == 0) return st;
+  st = validate_paged(*p, stride_page, page_size, num_pages, block_table, max_pages_per_seq, max_ctx_len);
+  if (st != COMEM_OK) return st;
+  if (p->device == COMEM_NO_DEVICE) return COMEM_ERR_NO_DEVICE;
+  a.block_table = block_table;
+  a.stride_page = stride_page * elem_bytes(p->cfg);
+  a.num_pages = num_pages;
+  a.max_pages = max_pages_per_seq;
+  a.page_shift = log2_of(page_size);
+  a.page_mask = page_size - 1;
+  return launch_append(a, true, batch, hip_stream);
 }
 
 }  // extern "C"

@@ -190,6 +190,59 @@ def test_paged_validation(plan, kw, status):
     assert B.load_library().comem_decode_attn_paged(*_paged_args(p, ws, **kw).values()) == status
 
 
+def _append_args(plan, **kw):
+    args = dict(plan=plan, new_k=A, new_v=A, k=A, v=A, stride_token=8 * 128, stride_head=128, seq_start=A,
+                ctx_lens=A, batch=2, max_ctx_len=4096, stream=None)
+    args.update(kw)
+    return args
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(), B.ERR_NO_DEVICE),
+    (dict(batch=0, new_k=None), B.OK),
+    (dict(batch=-1), B.ERR_INVALID_SHAPE),
+    (dict(batch=5), B.ERR_INVALID_SHAPE),
+    (dict(max_ctx_len=4097), B.ERR_INVALID_SHAPE),
+    (dict(new_k=None), B.ERR_NULL_POINTER),
+    (dict(new_v=None), B.ERR_NULL_POINTER),
+    (dict(k=None), B.ERR_NULL_POINTER),
+    (dict(v=None), B.ERR_NULL_POINTER),
+    (dict(ctx_lens=None), B.ERR_NULL_POINTER),
+    (dict(seq_start=None), B.ERR_NULL_POINTER),
+    (dict(stride_token=0), B.ERR_INVALID_SHAPE),
+    (dict(stride_head=0), B.ERR_INVALID_SHAPE),
+    (dict(stride_token=8 * 128 + 4), B.ERR_MISALIGNED),
+    (dict(new_k=A + 8), B.ERR_MISALIGNED),
+    (dict(new_v=A + 2), B.ERR_MISALIGNED),
+    (dict(k=A + 4), B.ERR_MISALIGNED),
+    (dict(seq_start=A + 4), B.ERR_MISALIGNED),
+])
+def test_append_validation(plan, kw, status):
+    p, _ = plan
+    assert B.load_library().comem_kv_append(*_append_args(p, **kw).values()) == status
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(), B.ERR_NO_DEVICE),
+    (dict(block_table=None), B.ERR_NULL_POINTER),
+    (dict(page_size=24), B.ERR_INVALID_SHAPE),
+    (dict(num_pages=0), B.ERR_INVALID_SHAPE),
+    (dict(max_pages=255), B.ERR_INVALID_SHAPE),
+    (dict(stride_page=16 * 8 * 128 + 4), B.ERR_MISALIGNED),
+    (dict(block_table=A + 2), B.ERR_MISALIGNED),
+    (dict(new_v=None), B.ERR_NULL_POINTER),
+    (dict(batch=0, block_table=None), B.OK),
+])
+def test_append_paged_validation(plan, kw, status):
+    p, _ = plan
+    args = dict(plan=p, new_k=A, new_v=A, k=A, v=A, stride_page=16 * 8 * 128, stride_token=8 * 128,
+                stride_head=128, page_size=16, num_pages=100, block_table=A, max_pages=256, ctx_lens=A, batch=2,
+                max_ctx_len=4096, stream=None)
+    args.update(kw)
+    assert B.load_library().comem_kv_append_paged(*args.values()) == status
+    assert B.load_library().comem_kv_append_paged(*dict(args, plan=None).values()) == B.ERR_BAD_HANDLE
+
+
 def test_forced_chunk_needs_room():
     p, ws = B.comem_decode_attn_init(_cfg(chunk_tokens=32), B.NO_DEVICE)
     try:

@@ -409,3 +409,28 @@ def test_mutant_widen_is_caught(monkeypatch):
 def test_mutant_cost_model_is_caught(monkeypatch):
     monkeypatch.setattr(cm, "max_compression_ratio", lambda W, Y, S, P: 1 / (1 + Y * S * P / W))
     assert _failing_pins()
+
+
+def test_append_then_context_is_concatenation():
+    """After appending, each sequence's logical context is the old one with the new row last (Sec. 2.2)."""
+    spec = small_spec(WORKLOADS[4], [1, 16, 17, 40], seed=50, max_ctx_len=64)
+    w = generate(spec, spare_pages=1)
+    r = np.random.default_rng(50)
+    new = f32_to_bf16_bits(r.standard_normal((4, spec.num_kv_heads, spec.head_dim)).astype(np.float32))
+    grown = w.ctx_lens  # lengths count the new token: its row is the last one of each context
+    after = da.append_paged(w.k_pages, w.block_table, grown, new)
+    for b in range(4):
+        before = da.paged_context(w.k_pages, w.block_table, grown, b)
+        ctx = da.paged_context(after, w.block_table, grown, b)
+        assert np.array_equal(ctx[:-1], before[:-1]) and np.array_equal(ctx[-1], new[b])
+    # every other pool row is untouched
+    changed = np.argwhere((after != w.k_pages).any(axis=(2, 3)))
+    assert len(changed) <= 4
+    spec_c = small_spec(WORKLOADS[2], [3, 0, 5], seed=51)
+    wc = generate(spec_c, gap_rows=2)
+    newc = f32_to_bf16_bits(r.standard_normal((3, 8, 128)).astype(np.float32))
+    afterc = da.append_contiguous(wc.k, wc.seq_start, wc.ctx_lens, newc)
+    assert np.array_equal(afterc[2], newc[0]) and np.array_equal(afterc[wc.seq_start[2] + 4], newc[2])
+    mask = np.ones(len(afterc), bool)
+    mask[[2, wc.seq_start[2] + 4]] = False
+    assert np.array_equal(afterc[mask], wc.k[mask])

@@ -254,6 +254,13 @@ def generate(spec: WorkloadSpec, seed: Optional[int] = None, *, gap_rows: int = 
     return Workload(spec, q, lens, k_pages=kp, v_pages=vp, block_table=bt)
 
 
+def draw_new_rows(spec: WorkloadSpec, seed: int):
+    """The new token's key and value rows for every sequence: two [B, Hkv, D] tensors ~ N(0,1) in spec.dtype."""
+    ks, vs = np.random.SeedSequence(seed).spawn(2)
+    shape = (spec.batch, spec.num_kv_heads, spec.head_dim)
+    return _draw_tensor(ks, shape, spec.dtype), _draw_tensor(vs, shape, spec.dtype)
+
+
 def small_spec(base: WorkloadSpec, lengths: Sequence[int], *, max_ctx_len: Optional[int] = None,
                seed: Optional[int] = None, **kw) -> WorkloadSpec:
     """A workload with the head shapes, dtype and layout of ``base`` but given lengths."""
