@@ -45,9 +45,9 @@ def _args():
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--workload", type=int, default=2, help="named workload 1..5 (2 = the headline one)")
-    ap.add_argument("--op", default="attention", choices=["attention", "append", "step"],
+    ap.add_argument("--op", default="attention", choices=["attention", "append", "step", "fused"],
                     help="attention: the decode-attention call; append: the KV-append call alone; "
-                         "step: append then attention, as one decode step runs them")
+                         "step: the append call then the attention call; fused: both in one launch")
     ap.add_argument("--variant", default="auto", choices=["auto", "mfma", "mfma_grid", "valu"])
     ap.add_argument("--chunk", type=int, default=0, help="tokens per split (0 = planned)")
     ap.add_argument("--copies", type=int, default=0, help="KV copies to cycle over (0 = enough to exceed the LLC)")
@@ -304,6 +304,14 @@ def main():
 
     def step(i, stream):
         k, v = kv[i % copies]
+        if a.op == "fused":  # the new token's rows are stored by the attention launch itself
+            if paged:
+                op.append_forward_paged(q, new_k, new_v, k, v, bt, ctx, spec.max_ctx_len, out=out, lse=lse,
+                                        stream=stream)
+            else:
+                op.append_forward(q, new_k, new_v, k, v, ss, ctx, spec.max_ctx_len, out=out, lse=lse,
+                                  stream=stream)
+            return
         if a.op != "attention":  # the new token's rows are stored first (same row on every step)
             if paged:
                 op.append_paged(new_k, new_v, k, v, bt, ctx, spec.max_ctx_len, stream=stream)

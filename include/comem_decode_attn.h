@@ -187,6 +187,33 @@ comem_status comem_kv_append_paged(const comem_decode_attn_plan* plan, const voi
                                    int32_t max_pages_per_seq, const int32_t* ctx_lens, int32_t batch,
                                    int64_t max_ctx_len, void* hip_stream);
 
+/* One decode step in one launch (paper Sec. 2.2: append, then attend): the
+ * same result as comem_kv_append followed by comem_decode_attn on one
+ * stream. The split that holds token L_b - 1 of each KV head stores that
+ * head's new K and V rows before it reads them; no other cache element is
+ * written. new_k, new_v: device [batch, h_kv, d_h] dense, dtype of the plan,
+ * 16-byte aligned. A sequence with ctx_lens[b] == 0 stores nothing. Unlike
+ * comem_kv_append, the device-side contract of the attention call applies
+ * (0 <= ctx_lens[b] <= max_ctx_len); only a block-table entry outside
+ * [0, num_pages) for token L_b - 1 skips the store. Other arguments as in
+ * comem_decode_attn. */
+comem_status comem_append_decode_attn(const comem_decode_attn_plan* plan, const void* q, const void* new_k,
+                                      const void* new_v, void* k, void* v, int64_t stride_token,
+                                      int64_t stride_head, const int64_t* seq_start, const int32_t* ctx_lens,
+                                      int32_t batch, int64_t max_ctx_len, float* out, float* lse,
+                                      void* workspace, size_t workspace_bytes, void* hip_stream);
+
+/* Paged form of comem_append_decode_attn; other arguments as in
+ * comem_decode_attn_paged. */
+comem_status comem_append_decode_attn_paged(const comem_decode_attn_plan* plan, const void* q,
+                                            const void* new_k, const void* new_v, void* k_pages,
+                                            void* v_pages, int64_t stride_page, int64_t stride_token,
+                                            int64_t stride_head, int32_t page_size, int64_t num_pages,
+                                            const int32_t* block_table, int32_t max_pages_per_seq,
+                                            const int32_t* ctx_lens, int32_t batch, int64_t max_ctx_len,
+                                            float* out, float* lse, void* workspace, size_t workspace_bytes,
+                                            void* hip_stream);
+
 #ifdef __cplusplus
 }
 #endif

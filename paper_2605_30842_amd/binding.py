@@ -28,7 +28,7 @@ NO_DEVICE = -1
 EXPORTED = (
     "comem_decode_attn_init", "comem_decode_attn_destroy", "comem_status_string",
     "comem_decode_attn_plan_splits", "comem_decode_attn", "comem_decode_attn_paged",
-    "comem_kv_append", "comem_kv_append_paged",
+    "comem_kv_append", "comem_kv_append_paged", "comem_append_decode_attn", "comem_append_decode_attn_paged",
 )
 PROBE_EXPORTED = ("comem_probe_read", "comem_probe_copy")
 
@@ -83,6 +83,11 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.comem_kv_append.restype = ctypes.c_int
     lib.comem_kv_append_paged.argtypes = [vp, vp, vp, vp, vp, i64, i64, i64, i32, i64, vp, i32, vp, i32, i64, vp]
     lib.comem_kv_append_paged.restype = ctypes.c_int
+    lib.comem_append_decode_attn.argtypes = [vp, vp, vp, vp, vp, vp, i64, i64, vp, vp, i32, i64, vp, vp, vp, sz, vp]
+    lib.comem_append_decode_attn.restype = ctypes.c_int
+    lib.comem_append_decode_attn_paged.argtypes = [vp, vp, vp, vp, vp, vp, i64, i64, i64, i32, i64, vp, i32, vp,
+                                                   i32, i64, vp, vp, vp, sz, vp]
+    lib.comem_append_decode_attn_paged.restype = ctypes.c_int
     _lib = lib
     return lib
 
@@ -184,6 +189,23 @@ def comem_kv_append_paged(plan, new_k, new_v, k_pages, v_pages, stride_page, str
            "comem_kv_append_paged")
 
 
+def comem_append_decode_attn(plan, q, new_k, new_v, k, v, stride_token, stride_head, seq_start, ctx_lens, batch,
+                             max_ctx_len, out, lse, workspace, workspace_bytes, stream) -> None:
+    _check(load_library().comem_append_decode_attn(plan, q, new_k, new_v, k, v, stride_token, stride_head,
+                                                   seq_start, ctx_lens, batch, max_ctx_len, out, lse, workspace,
+                                                   workspace_bytes, stream), "comem_append_decode_attn")
+
+
+def comem_append_decode_attn_paged(plan, q, new_k, new_v, k_pages, v_pages, stride_page, stride_token, stride_head,
+                                   page_size, num_pages, block_table, max_pages_per_seq, ctx_lens, batch,
+                                   max_ctx_len, out, lse, workspace, workspace_bytes, stream) -> None:
+    _check(load_library().comem_append_decode_attn_paged(plan, q, new_k, new_v, k_pages, v_pages, stride_page,
+                                                         stride_token, stride_head, page_size, num_pages,
+                                                         block_table, max_pages_per_seq, ctx_lens, batch,
+                                                         max_ctx_len, out, lse, workspace, workspace_bytes, stream),
+           "comem_append_decode_attn_paged")
+
+
 # ------------------------------------------------------------ torch wrapper
 
 
@@ -259,6 +281,30 @@ class DecodeAttention:
                               v_pages.data_ptr(), k_pages.stride(0), k_pages.stride(1), k_pages.stride(2),
                               k_pages.shape[1], k_pages.shape[0], block_table.data_ptr(), block_table.shape[1],
                               ctx_lens.data_ptr(), new_k.shape[0], int(max_ctx_len), self._stream(stream))
+
+    def append_forward(self, q, new_k, new_v, k, v, seq_start, ctx_lens, max_ctx_len: int, out=None, lse=None,
+                       stream=None):
+        """Store the new rows as token ctx_lens[b] - 1 and attend, in one launch."""
+        out, lse = self._outputs(q, out, lse)
+        assert k.stride() == v.stride() and k.stride(-1) == 1
+        comem_append_decode_attn(self.plan, q.data_ptr(), new_k.data_ptr(), new_v.data_ptr(), k.data_ptr(),
+                                 v.data_ptr(), k.stride(0), k.stride(1), seq_start.data_ptr(), ctx_lens.data_ptr(),
+                                 q.shape[0], int(max_ctx_len), out.data_ptr(),
+                                 None if lse is None else lse.data_ptr(), self.workspace.data_ptr(),
+                                 self.workspace_bytes, self._stream(stream))
+        return out, lse
+
+    def append_forward_paged(self, q, new_k, new_v, k_pages, v_pages, block_table, ctx_lens, max_ctx_len: int,
+                             out=None, lse=None, stream=None):
+        out, lse = self._outputs(q, out, lse)
+        assert k_pages.stride() == v_pages.stride() and k_pages.stride(-1) == 1
+        comem_append_decode_attn_paged(self.plan, q.data_ptr(), new_k.data_ptr(), new_v.data_ptr(),
+                                       k_pages.data_ptr(), v_pages.data_ptr(), k_pages.stride(0), k_pages.stride(1),
+                                       k_pages.stride(2), k_pages.shape[1], k_pages.shape[0], block_table.data_ptr(),
+                                       block_table.shape[1], ctx_lens.data_ptr(), q.shape[0], int(max_ctx_len),
+                                       out.data_ptr(), None if lse is None else lse.data_ptr(),
+                                       self.workspace.data_ptr(), self.workspace_bytes, self._stream(stream))
+        return out, lse
 
     def forward_paged(self, q, k_pages, v_pages, block_table, ctx_lens, max_ctx_len: int, out=None, lse=None,
                       stream=None):

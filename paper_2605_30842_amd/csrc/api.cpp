@@ -283,6 +283,79 @@ void fill_common(const comem_decode_attn_plan& p, comem::AttnParams& a, const vo
   }
 }
 
+// The attention calls, with or without the fused append of the new rows.
+comem_status decode_contiguous(const comem_decode_attn_plan* plan, const void* q, const void* new_k,
+                               const void* new_v, const void* k, const void* v, int64_t stride_token,
+                               int64_t stride_head, const int64_t* seq_start, const int32_t* ctx_lens,
+                               int32_t batch, int64_t max_ctx_len, float* out, float* lse, void* workspace,
+                               size_t workspace_bytes, void* hip_stream, bool fused) {
+  const comem_decode_attn_plan* p = checked(plan);
+  if (p == nullptr) return COMEM_ERR_BAD_HANDLE;
+  comem_status st = validate_common(*p, q, k, v, stride_token, stride_head, ctx_lens, batch, max_ctx_len,
+                                    out, lse, workspace);
+  if (st != COMEM_OK || batch == 0) return st;
+  if (seq_start == nullptr) return COMEM_ERR_NULL_POINTER;
+  if (!aligned(seq_start, 8)) return COMEM_ERR_MISALIGNED;
+  if (fused) {
+    if (new_k == nullptr || new_v == nullptr) return COMEM_ERR_NULL_POINTER;
+    if (!aligned(new_k, 16) || !aligned(new_v, 16)) return COMEM_ERR_MISALIGNED;
+  }
+  int64_t chunk = 0, splits = 0;
+  st = plan_call(*p, batch, max_ctx_len, workspace == nullptr ? 0 : workspace_bytes, &chunk, &splits);
+  if (st != COMEM_OK) return st;
+  if (p->device == COMEM_NO_DEVICE) return COMEM_ERR_NO_DEVICE;
+  const bool queue = uses_queue(*p, batch, workspace, workspace_bytes);
+  comem::AttnParams a;
+  fill_common(*p, a, q, k, v, stride_token, stride_head, ctx_lens, out, lse, workspace, batch, chunk, splits,
+              queue);
+  a.seq_start = seq_start;
+  if (fused) {
+    a.new_k = static_cast<const char*>(new_k);
+    a.new_v = static_cast<const char*>(new_v);
+  }
+  return launch(*p, false, a, batch, splits, queue, hip_stream);
+}
+
+comem_status decode_paged(const comem_decode_attn_plan* plan, const void* q, const void* new_k,
+                          const void* new_v, const void* k_pages, const void* v_pages, int64_t stride_page,
+                          int64_t stride_token, int64_t stride_head, int32_t page_size, int64_t num_pages,
+                          const int32_t* block_table, int32_t max_pages_per_seq, const int32_t* ctx_lens,
+                          int32_t batch, int64_t max_ctx_len, float* out, float* lse, void* workspace,
+                          size_t workspace_bytes, void* hip_stream, bool fused) {
+  const comem_decode_attn_plan* p = checked(plan);
+  if (p == nullptr) return COMEM_ERR_BAD_HANDLE;
+  comem_status st = validate_common(*p, q, k_pages, v_pages, stride_token, stride_head, ctx_lens, batch,
+                                    max_ctx_len, out, lse, workspace);
+  if (st != COMEM_OK || batch == 0) return st;
+  st = validate_paged(*p, stride_page, page_size, num_pages, block_table, max_pages_per_seq, max_ctx_len);
+  if (st != COMEM_OK) return st;
+  if (fused) {
+    if (new_k == nullptr || new_v == nullptr) return COMEM_ERR_NULL_POINTER;
+    if (!aligned(new_k, 16) || !aligned(new_v, 16)) return COMEM_ERR_MISALIGNED;
+  }
+  int64_t chunk = 0, splits = 0;
+  st = plan_call(*p, batch, max_ctx_len, workspace == nullptr ? 0 : workspace_bytes, &chunk, &splits);
+  if (st != COMEM_OK) return st;
+  // The matrix-core kernel stages one split's block-table entries in LDS.
+  if (uses_mfma(*p) && (chunk - 1) / page_size + 2 > comem::mfma_max_split_pages()) return COMEM_ERR_INVALID_SHAPE;
+  if (p->device == COMEM_NO_DEVICE) return COMEM_ERR_NO_DEVICE;
+  const bool queue = uses_queue(*p, batch, workspace, workspace_bytes);
+  comem::AttnParams a;
+  fill_common(*p, a, q, k_pages, v_pages, stride_token, stride_head, ctx_lens, out, lse, workspace, batch,
+              chunk, splits, queue);
+  a.block_table = block_table;
+  a.stride_page = stride_page * elem_bytes(p->cfg);
+  a.max_pages = max_pages_per_seq;
+  a.num_pages = num_pages;
+  a.page_shift = log2_of(page_size);
+  a.page_mask = page_size - 1;
+  if (fused) {
+    a.new_k = static_cast<const char*>(new_k);
+    a.new_v = static_cast<const char*>(new_v);
+  }
+  return launch(*p, true, a, batch, splits, queue, hip_stream);
+}
+
 }  // namespace
 
 extern "C" {
@@ -380,23 +453,8 @@ comem_status comem_decode_attn(const comem_decode_attn_plan* plan, const void* q
                                const int64_t* seq_start, const int32_t* ctx_lens, int32_t batch,
                                int64_t max_ctx_len, float* out, float* lse, void* workspace,
                                size_t workspace_bytes, void* hip_stream) {
-  const comem_decode_attn_plan* p = checked(plan);
-  if (p == nullptr) return COMEM_ERR_BAD_HANDLE;
-  comem_status st = validate_common(*p, q, k, v, stride_token, stride_head, ctx_lens, batch, max_ctx_len,
-                                    out, lse, workspace);
-  if (st != COMEM_OK || batch == 0) return st;
-  if (seq_start == nullptr) return COMEM_ERR_NULL_POINTER;
-  if (!aligned(seq_start, 8)) return COMEM_ERR_MISALIGNED;
-  int64_t chunk = 0, splits = 0;
-  st = plan_call(*p, batch, max_ctx_len, workspace == nullptr ? 0 : workspace_bytes, &chunk, &splits);
-  if (st != COMEM_OK) return st;
-  if (p->device == COMEM_NO_DEVICE) return COMEM_ERR_NO_DEVICE;
-  const bool queue = uses_queue(*p, batch, workspace, workspace_bytes);
-  comem::AttnParams a;
-  fill_common(*p, a, q, k, v, stride_token, stride_head, ctx_lens, out, lse, workspace, batch, chunk, splits,
-              queue);
-  a.seq_start = seq_start;
-  return launch(*p, false, a, batch, splits, queue, hip_stream);
+  return decode_contiguous(plan, q, nullptr, nullptr, k, v, stride_token, stride_head, seq_start, ctx_lens, batch,
+                           max_ctx_len, out, lse, workspace, workspace_bytes, hip_stream, false);
 }
 
 comem_status comem_decode_attn_paged(const comem_decode_attn_plan* plan, const void* q,
@@ -406,29 +464,31 @@ comem_status comem_decode_attn_paged(const comem_decode_attn_plan* plan, const v
                                      int32_t max_pages_per_seq, const int32_t* ctx_lens,
                                      int32_t batch, int64_t max_ctx_len, float* out, float* lse,
                                      void* workspace, size_t workspace_bytes, void* hip_stream) {
-  const comem_decode_attn_plan* p = checked(plan);
-  if (p == nullptr) return COMEM_ERR_BAD_HANDLE;
-  comem_status st = validate_common(*p, q, k_pages, v_pages, stride_token, stride_head, ctx_lens, batch,
-                                    max_ctx_len, out, lse, workspace);
-  if (st != COMEM_OK || batch == 0) return st;
-  st = validate_paged(*p, stride_page, page_size, num_pages, block_table, max_pages_per_seq, max_ctx_len);
-  if (st != COMEM_OK) return st;
-  int64_t chunk = 0, splits = 0;
-  st = plan_call(*p, batch, max_ctx_len, workspace == nullptr ? 0 : workspace_bytes, &chunk, &splits);
-  if (st != COMEM_OK) return st;
-  // The matrix-core kernel stages one split's block-table entries in LDS.
-  if (uses_mfma(*p) && (chunk - 1) / page_size + 2 > comem::mfma_max_split_pages()) return COMEM_ERR_INVALID_SHAPE;
-  if (p->device == COMEM_NO_DEVICE) return COMEM_ERR_NO_DEVICE;
-  const bool queue = uses_queue(*p, batch, workspace, workspace_bytes);
-  comem::AttnParams a;
-  fill_common(*p, a, q, k_pages, v_pages, stride_token, stride_head, ctx_lens, out, lse, workspace, batch,
-              chunk, splits, queue);
-  a.block_table = block_table;
-  a.stride_page = stride_page * elem_bytes(p->cfg);
-  a.max_pages = max_pages_per_seq;
-  a.page_shift = log2_of(page_size);
-  a.page_mask = page_size - 1;
-  return launch(*p, true, a, batch, splits, queue, hip_stream);
+  return decode_paged(plan, q, nullptr, nullptr, k_pages, v_pages, stride_page, stride_token, stride_head,
+                      page_size, num_pages, block_table, max_pages_per_seq, ctx_lens, batch, max_ctx_len, out, lse,
+                      workspace, workspace_bytes, hip_stream, false);
+}
+
+comem_status comem_append_decode_attn(const comem_decode_attn_plan* plan, const void* q, const void* new_k,
+                                      const void* new_v, void* k, void* v, int64_t stride_token,
+                                      int64_t stride_head, const int64_t* seq_start, const int32_t* ctx_lens,
+                                      int32_t batch, int64_t max_ctx_len, float* out, float* lse,
+                                      void* workspace, size_t workspace_bytes, void* hip_stream) {
+  return decode_contiguous(plan, q, new_k, new_v, k, v, stride_token, stride_head, seq_start, ctx_lens, batch,
+                           max_ctx_len, out, lse, workspace, workspace_bytes, hip_stream, true);
+}
+
+comem_status comem_append_decode_attn_paged(const comem_decode_attn_plan* plan, const void* q,
+                                            const void* new_k, const void* new_v, void* k_pages,
+                                            void* v_pages, int64_t stride_page, int64_t stride_token,
+                                            int64_t stride_head, int32_t page_size, int64_t num_pages,
+                                            const int32_t* block_table, int32_t max_pages_per_seq,
+                                            const int32_t* ctx_lens, int32_t batch, int64_t max_ctx_len,
+                                            float* out, float* lse, void* workspace, size_t workspace_bytes,
+                                            void* hip_stream) {
+  return decode_paged(plan, q, new_k, new_v, k_pages, v_pages, stride_page, stride_token, stride_head, page_size,
+                      num_pages, block_table, max_pages_per_seq, ctx_lens, batch, max_ctx_len, out, lse, workspace,
+                      workspace_bytes, hip_stream, true);
 }
 
 comem_status comem_kv_append(const comem_decode_attn_plan* plan, const void* new_k, const void* new_v,

@@ -54,6 +54,9 @@ struct AttnParams {
   int32_t queue_slot;  // index of the queue counters in tickets
   float* lse_part;     // [B, Hkv, S, G]   (log2 units)
   float* o_part;       // [B, Hkv, S, G, D]
+  const char* new_k;   // fused append: new rows [B, Hkv, D], or nullptr for attention only
+  const char* new_v;
+  int64_t num_pages;   // paged layout: pool size (bounds the fused append's store)
 };
 
 // Per-wave partial state handed from the token loop to the finalize step.
@@ -87,6 +90,35 @@ __device__ inline int64_t row_offset(const AttnParams& p, int b, int64_t seq0, i
 }
 
 __device__ inline float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
+// Fused KV append (paper Sec. 2.2: the new token's key and value join the
+// caches before it attends). Called by the one wave of the split holding
+// token L - 1 that will also load that token's row, before any of its loads:
+// `pieces` lanes store the K row of head hk, the next `pieces` lanes the V
+// row (16 bytes each; 2 * pieces <= 64). Memory operations of one wave to
+// one address take effect in program order, so the wave's later loads of
+// the row return the new values without a wait; the wavefront-scope fence
+// keeps the compiler from moving those loads above the stores. row_off < 0
+// (a page outside the pool) skips the store.
+__device__ inline void store_new_token(const AttnParams& p, int b, int hk, int64_t row_off, int pieces,
+                                       int lane) {
+  if (row_off >= 0 && lane < 2 * pieces) {
+    const bool is_v = lane >= pieces;
+    const int piece = is_v ? lane - pieces : lane;
+    const int64_t src = (static_cast<int64_t>(b) * p.num_kv_heads + hk) * pieces * 16 + piece * 16;
+    const uint4 val = *reinterpret_cast<const uint4*>((is_v ? p.new_v : p.new_k) + src);
+    char* dst = const_cast<char*>(is_v ? p.v : p.k) + hk * p.stride_head + row_off + piece * 16;
+    *reinterpret_cast<uint4*>(dst) = val;
+  }
+  __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+}
+
+// Paged layout: byte offset of the page slot of token t, or -1 when the
+// block-table entry lies outside the pool.
+__device__ inline int64_t checked_page_row(const AttnParams& p, int32_t page, int t) {
+  if (page < 0 || page >= p.num_pages) return -1;
+  return static_cast<int64_t>(page) * p.stride_page + static_cast<int64_t>(t & p.page_mask) * p.stride_token;
+}
 
 // Partial results cross workgroups that may run on different XCDs, whose L2
 // caches are not coherent with each other. They are written and read with

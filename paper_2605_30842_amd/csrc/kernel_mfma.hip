@@ -298,6 +298,16 @@ __device__ void attend_split(const AttnParams& p, SplitSmem<D, LAYOUT>& sm, int 
   const int ntok = t_end - t_begin;
   const int nfull = ntok >> 5;              // full 32-token tiles
   const int ntiles = (ntok + 31) >> 5;      // including a partial last tile
+  // Fused append: the wave that owns the tile of token L - 1 stores its rows first.
+  if (p.new_k != nullptr && t_end == L && L > 0 && w == (ntiles - 1) % kWaves) {
+    int64_t row;
+    if constexpr (LAYOUT == Layout::kContig) {
+      row = p.seq_start[b] * p.stride_token + static_cast<int64_t>(L - 1) * p.stride_token;
+    } else {
+      row = checked_page_row(p, sm.pages[((L - 1) - ld.page_first) >> p.page_shift], L - 1);
+    }
+    store_new_token(p, b, hk, row, D / 8, lane);
+  }
   int ti = w;
   if constexpr (LAYOUT != Layout::kPagedFine) {
     // Full tiles w, w + 4, ...: while one tile is computed the next is in

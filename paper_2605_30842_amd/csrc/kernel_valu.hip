@@ -83,6 +83,18 @@ __global__ __launch_bounds__(kThreads) void decode_valu_kernel(const AttnParams 
   }
 
   const int ntok = t_end - t_begin;
+  // Fused append: the wave whose tile holds token L - 1 (and every clamped
+  // read of that row) stores the new rows first.
+  if (p.new_k != nullptr && t_end == L && L > 0 && w == ((L - 1 - t_begin) / TT) % kWaves) {
+    int64_t row;
+    if constexpr (PAGED) {
+      row = checked_page_row(p, p.block_table[static_cast<int64_t>(b) * p.max_pages + ((L - 1) >> p.page_shift)],
+                             L - 1);
+    } else {
+      row = (seq0 + L - 1) * p.stride_token;
+    }
+    store_new_token(p, b, hk, row, D * EB / 16, lane);
+  }
   for (int base = t_begin + w * TT; base < t_begin + ntok; base += kWaves * TT) {
     u32x4 kr[U], vr[U];
 #pragma unroll

@@ -243,6 +243,29 @@ def test_append_paged_validation(plan, kw, status):
     assert B.load_library().comem_kv_append_paged(*dict(args, plan=None).values()) == B.ERR_BAD_HANDLE
 
 
+@pytest.mark.parametrize("kw,status", [
+    (dict(), B.ERR_NO_DEVICE),
+    (dict(new_k=None), B.ERR_NULL_POINTER),
+    (dict(new_v=None), B.ERR_NULL_POINTER),
+    (dict(new_k=A + 8), B.ERR_MISALIGNED),
+    (dict(q=None), B.ERR_NULL_POINTER),
+    (dict(batch=0, new_k=None), B.OK),
+    (dict(batch=5), B.ERR_INVALID_SHAPE),
+])
+def test_fused_append_validation(plan, kw, status):
+    p, ws = plan
+    c = _contig_args(p, ws)
+    args = dict(plan=p, q=A, new_k=A, new_v=A)
+    args.update({k: c[k] for k in c if k not in ("plan", "q")})
+    args.update(kw)
+    assert B.load_library().comem_append_decode_attn(*args.values()) == status
+    g = _paged_args(p, ws)
+    pargs = dict(plan=p, q=A, new_k=A, new_v=A)
+    pargs.update({k: g[k] for k in g if k not in ("plan", "q")})
+    pargs.update(kw)
+    assert B.load_library().comem_append_decode_attn_paged(*pargs.values()) == status
+
+
 def test_forced_chunk_needs_room():
     p, ws = B.comem_decode_attn_init(_cfg(chunk_tokens=32), B.NO_DEVICE)
     try:

@@ -101,6 +101,58 @@ def test_append_bitwise_then_attend(name, base, lens, kw):
     check(out, lse, ro, rl, spec.dtype, f"{name} attention after append")
 
 
+FUSED = [
+    ("contig_f32", 1, [1, 31, 32, 33, 0, 1000], {}, "auto", 0),
+    ("contig_bf16_mfma", 2, [1, 0, 32, 33, 100, 4097], {"gap_rows": 3}, "mfma", 0),
+    ("contig_bf16_grid_c32", 2, [1, 0, 32, 33, 100, 4097], {}, "mfma_grid", 32),
+    ("contig_bf16_valu", 2, [1, 0, 32, 33, 100, 4097], {}, "valu", 0),
+    ("paged16_mfma", 4, [1, 15, 16, 17, 0, 300], {"spare_pages": 5}, "mfma", 0),
+    ("paged16_valu", 4, [1, 15, 16, 17, 0, 300], {}, "valu", 64),
+    ("paged1", 4, [1, 2, 3, 64], {"page_size": 1}, "mfma", 0),
+    ("paged64_g8", 5, [63, 64, 65, 1000], {}, "mfma", 0),
+    ("paged16_queue", 4, [1000 + 37 * i for i in range(16)], {}, "mfma", 32),
+]
+
+
+@pytest.mark.parametrize("name,base,lens,kw,variant,chunk", FUSED, ids=[c[0] for c in FUSED])
+def test_fused_append_attend(name, base, lens, kw, variant, chunk):
+    """One launch appends and attends: same cache bits as the oracle's append, and the same output bits
+    as the separate append call followed by the attention call."""
+    import torch
+
+    gen = {k: kw[k] for k in ("gap_rows", "spare_pages") if k in kw}
+    spec_kw = {k: v for k, v in kw.items() if k not in gen}
+    spec = small_spec(WORKLOADS[base], lens, seed=330 + base, **spec_kw)
+    w = generate(spec, **gen)
+    new_k, new_v = draw_new_rows(spec, seed=430 + base)
+    say(f"case fused {name} lens={lens[:6]} {spec.dtype} {spec.layout} ps={spec.page_size} {variant} chunk={chunk}")
+    op = make_op(spec, chunk=chunk, variant=variant)
+    nk, nv = to_torch(new_k, spec.dtype, "cuda:0"), to_torch(new_v, spec.dtype, "cuda:0")
+    fused = DeviceWorkload(w)
+    lse = torch.empty((spec.batch, spec.num_q_heads), dtype=torch.float32, device="cuda:0")
+    if spec.layout == "paged":
+        out, lse = op.append_forward_paged(fused.q, nk, nv, fused.k, fused.v, fused.block_table, fused.ctx_lens,
+                                           spec.max_ctx_len, lse=lse)
+    else:
+        out, lse = op.append_forward(fused.q, nk, nv, fused.k, fused.v, fused.seq_start, fused.ctx_lens,
+                                     spec.max_ctx_len, lse=lse)
+    torch.cuda.synchronize()
+    want_k, want_v = _oracle_append(w, new_k, new_v)
+    _bitwise(_host(fused.k, spec.dtype), want_k, f"{name} K cache")
+    _bitwise(_host(fused.v, spec.dtype), want_v, f"{name} V cache")
+    sep = DeviceWorkload(w)
+    _append(sep, op, new_k, new_v)
+    out2, lse2 = run(sep, op)
+    _bitwise(out.cpu().numpy(), out2, f"{name} out fused vs separate")
+    _bitwise(lse.cpu().numpy(), lse2, f"{name} lse fused vs separate")
+    if spec.layout == "paged":
+        w.k_pages, w.v_pages = want_k, want_v
+    else:
+        w.k, w.v = want_k, want_v
+    ro, rl = da.reference(w)
+    check(out.cpu().numpy(), lse.cpu().numpy(), ro, rl, spec.dtype, f"{name} fused vs oracle")
+
+
 def test_append_twice_grows_context():
     """Two decode steps: append at L, attend; append at L + 1, attend (lengths grow by one)."""
     import torch
