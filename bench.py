@@ -59,7 +59,7 @@ def _args():
     ap.add_argument("--probe-bytes", type=int, default=4 << 30)
     ap.add_argument("--probe-blocks", type=int, default=4096)
     ap.add_argument("--summarize", metavar="DIR", default=None,
-                    help="write profiles/ summaries from rocprofv3 outputs under DIR (see profiles/README.md)")
+                    help="write profiles/ summaries from rocprofv3 outputs under DIR (layout in summarize())")
     return ap.parse_args()
 
 
@@ -343,12 +343,15 @@ def main():
     steps = a.steps
     ms = eager_ms
     if a.timing == "graph":
-        # One graph holds one launch per KV copy; the timed region replays it.
+        # One graph holds at least 16 launches, cycling over the KV copies, so
+        # the gap between graph launches is spread over many steps; the timed
+        # region replays it.
+        per_graph = copies * max(1, -(-16 // copies))
         graph = torch.cuda.CUDAGraph()
         side = torch.cuda.Stream()
         side.wait_stream(stream)
         with torch.cuda.graph(graph, stream=side):
-            for i in range(copies):
+            for i in range(per_graph):
                 step(i, torch.cuda.current_stream())
         torch.cuda.synchronize()
         for _ in range(3):  # every replay must reproduce the eager result bit for bit
@@ -356,8 +359,8 @@ def main():
             graph.replay()
             torch.cuda.synchronize()
             assert torch.equal(out, eager_out), "graph replay differs from eager result"
-        replays = max(1, -(-a.steps // copies))
-        steps = replays * copies
+        replays = max(1, -(-a.steps // per_graph))
+        steps = replays * per_graph
         ms = timed(lambda: [graph.replay() for _ in range(replays)], steps)
     if a.op == "append":
         row_bytes = spec.batch * spec.num_kv_heads * spec.head_dim * spec.elem_bytes * 2  # K and V rows

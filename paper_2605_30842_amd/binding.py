@@ -31,6 +31,10 @@ EXPORTED = (
     "comem_kv_append", "comem_kv_append_paged", "comem_append_decode_attn", "comem_append_decode_attn_paged",
 )
 PROBE_EXPORTED = ("comem_probe_read", "comem_probe_copy")
+COST_EXPORTED = (
+    "comem_cost_kv_bytes_per_token", "comem_cost_decode_time", "comem_cost_decode_saving",
+    "comem_cost_prefill_time", "comem_cost_net_saving", "comem_cost_max_compression_ratio",
+)
 
 
 class Config(ctypes.Structure):
@@ -44,6 +48,17 @@ class Config(ctypes.Structure):
         ("max_ctx_len", ctypes.c_int64),
         ("chunk_tokens", ctypes.c_int32),
         ("variant", ctypes.c_int32),
+    ]
+
+
+class CostInputs(ctypes.Structure):
+    """S (KV bytes per token), W (bytes/s), P (prefill tokens/s), Y (generated tokens)."""
+
+    _fields_ = [
+        ("kv_bytes_per_token", ctypes.c_double),
+        ("hbm_bytes_per_s", ctypes.c_double),
+        ("prefill_tokens_per_s", ctypes.c_double),
+        ("generated_tokens", ctypes.c_double),
     ]
 
 
@@ -83,6 +98,15 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.comem_kv_append.restype = ctypes.c_int
     lib.comem_kv_append_paged.argtypes = [vp, vp, vp, vp, vp, i64, i64, i64, i32, i64, vp, i32, vp, i32, i64, vp]
     lib.comem_kv_append_paged.restype = ctypes.c_int
+    dp, cp, f64 = ctypes.POINTER(ctypes.c_double), ctypes.POINTER(CostInputs), ctypes.c_double
+    lib.comem_cost_kv_bytes_per_token.argtypes = [i32, i32, i32, i32, dp]
+    lib.comem_cost_decode_time.argtypes = [cp, f64, dp]
+    lib.comem_cost_decode_saving.argtypes = [cp, f64, f64, dp]
+    lib.comem_cost_prefill_time.argtypes = [cp, f64, dp]
+    lib.comem_cost_net_saving.argtypes = [cp, f64, f64, dp]
+    lib.comem_cost_max_compression_ratio.argtypes = [cp, dp]
+    for name in COST_EXPORTED:
+        getattr(lib, name).restype = ctypes.c_int
     lib.comem_append_decode_attn.argtypes = [vp, vp, vp, vp, vp, vp, i64, i64, vp, vp, i32, i64, vp, vp, vp, sz, vp]
     lib.comem_append_decode_attn.restype = ctypes.c_int
     lib.comem_append_decode_attn_paged.argtypes = [vp, vp, vp, vp, vp, vp, i64, i64, i64, i32, i64, vp, i32, vp,
@@ -204,6 +228,36 @@ def comem_append_decode_attn_paged(plan, q, new_k, new_v, k_pages, v_pages, stri
                                                          block_table, max_pages_per_seq, ctx_lens, batch,
                                                          max_ctx_len, out, lse, workspace, workspace_bytes, stream),
            "comem_append_decode_attn_paged")
+
+
+def _cost_call(name, *args) -> float:
+    out = ctypes.c_double()
+    _check(getattr(load_library(), name)(*args, ctypes.byref(out)), name)
+    return out.value
+
+
+def comem_cost_kv_bytes_per_token(num_layers, num_kv_heads, head_dim, elem_bytes) -> float:
+    return _cost_call("comem_cost_kv_bytes_per_token", num_layers, num_kv_heads, head_dim, elem_bytes)
+
+
+def comem_cost_decode_time(inputs: CostInputs, ctx_tokens) -> float:
+    return _cost_call("comem_cost_decode_time", ctypes.byref(inputs), float(ctx_tokens))
+
+
+def comem_cost_decode_saving(inputs: CostInputs, l_full, l_sum) -> float:
+    return _cost_call("comem_cost_decode_saving", ctypes.byref(inputs), float(l_full), float(l_sum))
+
+
+def comem_cost_prefill_time(inputs: CostInputs, l_sum) -> float:
+    return _cost_call("comem_cost_prefill_time", ctypes.byref(inputs), float(l_sum))
+
+
+def comem_cost_net_saving(inputs: CostInputs, l_full, l_sum) -> float:
+    return _cost_call("comem_cost_net_saving", ctypes.byref(inputs), float(l_full), float(l_sum))
+
+
+def comem_cost_max_compression_ratio(inputs: CostInputs) -> float:
+    return _cost_call("comem_cost_max_compression_ratio", ctypes.byref(inputs))
 
 
 # ------------------------------------------------------------ torch wrapper
