@@ -100,3 +100,22 @@ def test_kv_bytes_formula(i):
     spec = WORKLOADS[i]
     lens = synth.draw_lengths(spec, np.random.default_rng(np.random.SeedSequence(spec.seed).spawn(6)[0]))
     assert int(lens.sum()) * 8 * 128 * 2 * 2 == (134217728 if i == 2 else int(lens.sum()) * 4096)
+
+
+def test_prefill_workloads_recipe():
+    """New-token counts stay within the context, queries are packed, and the K/V side equals the decode draw."""
+    from workloads.synth import PREFILL_WORKLOADS, generate, generate_prefill, small_prefill_spec
+
+    spec = small_prefill_spec(PREFILL_WORKLOADS[3], [40, 7, 300], [50, 7, 128], seed=9)
+    pw = generate_prefill(spec)
+    assert pw.q_lens.tolist() == [40, 7, 128]  # capped at L_b
+    assert pw.q_start.tolist() == [0, 40, 47]
+    assert pw.q.shape == (175, 32, 128) and pw.q.dtype == np.uint16
+    again = generate_prefill(spec)
+    assert np.array_equal(again.q, pw.q)
+    kv = generate(spec.kv, seed=9)
+    assert np.array_equal(kv.k_pages, pw.kv.k_pages) and np.array_equal(kv.block_table, pw.kv.block_table)
+    full = generate_prefill(PREFILL_WORKLOADS[2].__class__(
+        "x", PREFILL_WORKLOADS[2].kv.replace(lengths=("fixed", 64), max_ctx_len=64), ("all",), seed=4))
+    assert full.q_lens.tolist() == [64]
+    assert full.score_count == 64 * 65 // 2

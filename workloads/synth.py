@@ -261,6 +261,99 @@ def draw_new_rows(spec: WorkloadSpec, seed: int):
     return _draw_tensor(ks, shape, spec.dtype), _draw_tensor(vs, shape, spec.dtype)
 
 
+# ---------------------------------------------------------------- prefill workloads
+
+
+@dataclasses.dataclass(frozen=True)
+class PrefillSpec:
+    """A cached-prefix prefill workload: the KV side is a WorkloadSpec whose
+    lengths L_b count every cached token, the last M_b of them new.
+
+    new_tokens: ("fixed", M), ("uniform", lo, hi), ("list", (M0, ...)) or
+    ("all",) for M_b = L_b (an uncached prefill). M_b is capped at L_b.
+    """
+
+    name: str
+    kv: WorkloadSpec
+    new_tokens: tuple
+    seed: int = 0
+
+
+@dataclasses.dataclass
+class PrefillWorkload:
+    spec: PrefillSpec
+    kv: Workload       # K/V, lengths, layout (its q is unused)
+    q: np.ndarray      # [sum_b M_b, Hq, D], sequence b at q_start[b]
+    q_start: np.ndarray  # int64 [B]
+    q_lens: np.ndarray   # int32 [B]
+
+    @property
+    def score_count(self) -> int:
+        """Visible (query token, key) pairs per query head: sum_b sum_i (L_b - M_b + i + 1)."""
+        L = self.kv.ctx_lens.astype(np.int64)
+        M = self.q_lens.astype(np.int64)
+        return int(((L - M) * M + M * (M + 1) // 2).sum())
+
+    @property
+    def flops(self) -> int:
+        """Algorithmic flops: 2 D for q.k and 2 D for p.v per visible pair and query head."""
+        s = self.kv.spec
+        return 4 * s.head_dim * s.num_q_heads * self.score_count
+
+
+PREFILL_WORKLOADS = {
+    1: PrefillSpec("bf16_prefill_B1_P32768_M1024",
+                   WorkloadSpec("kv_B1_L33792", 1, 32, 8, 128, "bf16", ("fixed", 33792), 33792, seed=2001),
+                   ("fixed", 1024), seed=2001),
+    2: PrefillSpec("bf16_prefill_uncached_B1_L8192",
+                   WorkloadSpec("kv_B1_L8192", 1, 32, 8, 128, "bf16", ("fixed", 8192), 8192, seed=2002),
+                   ("all",), seed=2002),
+    3: PrefillSpec("bf16_prefill_paged16_B8_L8k-32k_M128-2048",
+                   WorkloadSpec("kv_B8_L8k-32k_paged16", 8, 32, 8, 128, "bf16", ("uniform", 8192, 32768), 32768,
+                                layout="paged", page_size=16, seed=2003),
+                   ("uniform", 128, 2048), seed=2003),
+}
+
+
+def generate_prefill(spec: PrefillSpec, seed: Optional[int] = None, **kv_kw) -> PrefillWorkload:
+    """Draw the K/V side with ``generate`` (same recipe), then the new-token counts and queries.
+
+    The counts and queries come from ``SeedSequence((seed, 1)).spawn(2)``, so
+    the K/V side equals the decode draw of the same KV spec and seed.
+    """
+    seed = spec.seed if seed is None else seed
+    kv = generate(spec.kv, seed=seed, **kv_kw)
+    lens_ss, q_ss = np.random.SeedSequence((seed, 1)).spawn(2)
+    rng = np.random.default_rng(lens_ss)
+    B = spec.kv.batch
+    kind = spec.new_tokens[0]
+    if kind == "all":
+        m = kv.ctx_lens.astype(np.int64)
+    elif kind == "fixed":
+        m = np.full(B, spec.new_tokens[1], dtype=np.int64)
+    elif kind == "uniform":
+        m = rng.integers(spec.new_tokens[1], spec.new_tokens[2], size=B, endpoint=True)
+    elif kind == "list":
+        m = np.asarray(spec.new_tokens[1], dtype=np.int64)
+    else:
+        raise ValueError(f"unknown new-token kind {kind!r}")
+    m = np.minimum(m, kv.ctx_lens.astype(np.int64)).astype(np.int32)
+    q_start = np.zeros(B, dtype=np.int64)
+    q_start[1:] = np.cumsum(m.astype(np.int64))[:-1]
+    total = int(m.astype(np.int64).sum())
+    s = spec.kv
+    q = _draw_tensor(q_ss, (max(total, 1), s.num_q_heads, s.head_dim), s.dtype)[:total]
+    return PrefillWorkload(spec, kv, q, q_start, m)
+
+
+def small_prefill_spec(base: PrefillSpec, ctx_lens: Sequence[int], new_tokens: Sequence[int], *,
+                       seed: Optional[int] = None, **kw) -> PrefillSpec:
+    """A prefill workload with the head shapes, dtype and layout of ``base`` but given lengths."""
+    kv = small_spec(base.kv, ctx_lens, seed=seed, **kw)
+    return PrefillSpec(base.name + "_small", kv, ("list", tuple(int(x) for x in new_tokens)),
+                       seed=kv.seed if seed is None else seed)
+
+
 def small_spec(base: WorkloadSpec, lengths: Sequence[int], *, max_ctx_len: Optional[int] = None,
                seed: Optional[int] = None, **kw) -> WorkloadSpec:
     """A workload with the head shapes, dtype and layout of ``base`` but given lengths."""
