@@ -223,6 +223,17 @@ __device__ inline void compute_tile(const Tile<D>& T, int t0, int t_end, int c, 
   }
 }
 
+// ctx_lens[b] and, for the contiguous layout, seq_start[b]: both loads are
+// issued before either value is used (the empty asm consumes both at once),
+// so they share one memory round trip.
+template <Layout LAYOUT>
+__device__ inline void load_sequence(const AttnParams& p, int b, int& L, int64_t& seq_row) {
+  b = uniform_i32(b);  // uniform in every caller
+  L = uniform_i32(p.ctx_lens[b]);
+  seq_row = LAYOUT == Layout::kContig ? uniform_i64(p.seq_start[b]) : 0;
+  asm volatile("" : "+s"(L), "+s"(seq_row));
+}
+
 // Shared memory of one workgroup; the page table and the wave states are
 // rewritten for every split the workgroup processes.
 template <int D, Layout LAYOUT>
@@ -234,13 +245,16 @@ struct SplitSmem {
 // Attention of the G query heads of KV head hk of sequence b over split j
 // (tokens [j * chunk, min((j + 1) * chunk, L))), ending with this split's
 // share of the log-sum-exp merge. Called by every thread of the workgroup.
+// seq_row is seq_start[b] for the contiguous layout (unused when paged); the
+// callers load it together with ctx_lens[b], so the two loads cost one
+// round trip before the first tile is requested.
 //
 // With next_item set (work-queue form), thread 0 takes the workgroup's next
 // item from the queue once the token loop is done: issued earlier, the queue
 // atomic would sit ahead of the tile loads in the in-order memory counter.
 template <int D, Layout LAYOUT>
 __device__ void attend_split(const AttnParams& p, SplitSmem<D, LAYOUT>& sm, int b, int hk, int j, int L,
-                             int* next_item) {
+                             int64_t seq_row, int* next_item) {
   constexpr int KB = D / 32;
   constexpr int NT = D / 16;
   const int nsplit_b = L > 0 ? 1 + (L - 1) / p.chunk : 1;
@@ -255,7 +269,7 @@ __device__ void attend_split(const AttnParams& p, SplitSmem<D, LAYOUT>& sm, int 
   ld.kbase = p.k + hk * p.stride_head;
   ld.vbase = p.v + hk * p.stride_head;
   if constexpr (LAYOUT == Layout::kContig) {
-    const int64_t seq0 = p.seq_start[b] * p.stride_token;
+    const int64_t seq0 = seq_row * p.stride_token;
     ld.kbase += seq0;
     ld.vbase += seq0;
   } else {
@@ -302,7 +316,7 @@ __device__ void attend_split(const AttnParams& p, SplitSmem<D, LAYOUT>& sm, int 
   if (p.new_k != nullptr && t_end == L && L > 0 && w == (ntiles - 1) % kWaves) {
     int64_t row;
     if constexpr (LAYOUT == Layout::kContig) {
-      row = p.seq_start[b] * p.stride_token + static_cast<int64_t>(L - 1) * p.stride_token;
+      row = (seq_row + static_cast<int64_t>(L - 1)) * p.stride_token;
     } else {
       row = checked_page_row(p, sm.pages[((L - 1) - ld.page_first) >> p.page_shift], L - 1);
     }
@@ -372,11 +386,13 @@ __device__ void attend_split(const AttnParams& p, SplitSmem<D, LAYOUT>& sm, int 
 template <int D, Layout LAYOUT>
 __global__ __launch_bounds__(kThreads, 2) void decode_mfma_kernel(const AttnParams p) {
   const int j = blockIdx.x, hk = blockIdx.y, b = blockIdx.z;
-  const int L = p.ctx_lens[b];
+  int L;
+  int64_t seq_row;
+  load_sequence<LAYOUT>(p, b, L, seq_row);
   const int nsplit_b = L > 0 ? 1 + (L - 1) / p.chunk : 1;
   if (j >= nsplit_b) return;
   __shared__ SplitSmem<D, LAYOUT> sm;
-  attend_split<D, LAYOUT>(p, sm, b, hk, j, L, nullptr);
+  attend_split<D, LAYOUT>(p, sm, b, hk, j, L, seq_row, nullptr);
 }
 
 // Persistent workgroups that take work items from a queue. Item i stands for
@@ -434,7 +450,10 @@ __global__ __launch_bounds__(kThreads, 2) void decode_mfma_queue_kernel(const At
       if (sm_first[mid] <= split_index) lo = mid; else hi = mid - 1;
     }
     const int b = lo;
-    attend_split<D, LAYOUT>(p, sm, b, hk, split_index - sm_first[b], p.ctx_lens[b], queued ? &sm_next : nullptr);
+    int L;
+    int64_t seq_row;
+    load_sequence<LAYOUT>(p, b, L, seq_row);
+    attend_split<D, LAYOUT>(p, sm, b, hk, split_index - sm_first[b], L, seq_row, queued ? &sm_next : nullptr);
     __syncthreads();
     item = queued ? sm_next : total;
     __syncthreads();
