@@ -29,6 +29,7 @@ EXPORTED = (
     "comem_decode_attn_init", "comem_decode_attn_destroy", "comem_status_string",
     "comem_decode_attn_plan_splits", "comem_decode_attn", "comem_decode_attn_paged",
     "comem_kv_append", "comem_kv_append_paged", "comem_append_decode_attn", "comem_append_decode_attn_paged",
+    "comem_prefill_attn", "comem_prefill_attn_paged",
 )
 PROBE_EXPORTED = ("comem_probe_read", "comem_probe_copy")
 COST_EXPORTED = (
@@ -112,6 +113,11 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.comem_append_decode_attn_paged.argtypes = [vp, vp, vp, vp, vp, vp, i64, i64, i64, i32, i64, vp, i32, vp,
                                                    i32, i64, vp, vp, vp, sz, vp]
     lib.comem_append_decode_attn_paged.restype = ctypes.c_int
+    lib.comem_prefill_attn.argtypes = [vp, vp, vp, vp, i32, vp, vp, i64, i64, vp, vp, i32, i64, vp, vp, vp]
+    lib.comem_prefill_attn.restype = ctypes.c_int
+    lib.comem_prefill_attn_paged.argtypes = [vp, vp, vp, vp, i32, vp, vp, i64, i64, i64, i32, i64, vp, i32, vp,
+                                             i32, i64, vp, vp, vp]
+    lib.comem_prefill_attn_paged.restype = ctypes.c_int
     _lib = lib
     return lib
 
@@ -228,6 +234,23 @@ def comem_append_decode_attn_paged(plan, q, new_k, new_v, k_pages, v_pages, stri
                                                          block_table, max_pages_per_seq, ctx_lens, batch,
                                                          max_ctx_len, out, lse, workspace, workspace_bytes, stream),
            "comem_append_decode_attn_paged")
+
+
+def comem_prefill_attn(plan, q, q_start, q_lens, max_q_len, k, v, stride_token, stride_head, seq_start, ctx_lens,
+                       batch, max_ctx_len, out, lse, stream) -> None:
+    _check(load_library().comem_prefill_attn(plan, q, q_start, q_lens, max_q_len, k, v, stride_token, stride_head,
+                                             seq_start, ctx_lens, batch, max_ctx_len, out, lse, stream),
+           "comem_prefill_attn")
+
+
+def comem_prefill_attn_paged(plan, q, q_start, q_lens, max_q_len, k_pages, v_pages, stride_page, stride_token,
+                             stride_head, page_size, num_pages, block_table, max_pages_per_seq, ctx_lens, batch,
+                             max_ctx_len, out, lse, stream) -> None:
+    _check(load_library().comem_prefill_attn_paged(plan, q, q_start, q_lens, max_q_len, k_pages, v_pages,
+                                                   stride_page, stride_token, stride_head, page_size, num_pages,
+                                                   block_table, max_pages_per_seq, ctx_lens, batch, max_ctx_len,
+                                                   out, lse, stream),
+           "comem_prefill_attn_paged")
 
 
 def _cost_call(name, *args) -> float:
@@ -370,4 +393,33 @@ class DecodeAttention:
                                 ctx_lens.data_ptr(), q.shape[0], int(max_ctx_len), out.data_ptr(),
                                 None if lse is None else lse.data_ptr(), self.workspace.data_ptr(),
                                 self.workspace_bytes, self._stream(stream))
+        return out, lse
+
+    def _prefill_outputs(self, q, out, lse):
+        import torch
+
+        if out is None:
+            out = torch.empty(q.shape, dtype=torch.float32, device=q.device)
+        return out, lse
+
+    def prefill(self, q, q_start, q_lens, max_q_len: int, k, v, seq_start, ctx_lens, max_ctx_len: int, out=None,
+                lse=None, stream=None):
+        """Prefill attention of the packed new tokens q [total, Hq, D] over a contiguous cache."""
+        out, lse = self._prefill_outputs(q, out, lse)
+        assert k.stride() == v.stride() and k.stride(-1) == 1
+        comem_prefill_attn(self.plan, q.data_ptr(), q_start.data_ptr(), q_lens.data_ptr(), int(max_q_len),
+                           k.data_ptr(), v.data_ptr(), k.stride(0), k.stride(1), seq_start.data_ptr(),
+                           ctx_lens.data_ptr(), ctx_lens.shape[0], int(max_ctx_len), out.data_ptr(),
+                           None if lse is None else lse.data_ptr(), self._stream(stream))
+        return out, lse
+
+    def prefill_paged(self, q, q_start, q_lens, max_q_len: int, k_pages, v_pages, block_table, ctx_lens,
+                      max_ctx_len: int, out=None, lse=None, stream=None):
+        out, lse = self._prefill_outputs(q, out, lse)
+        assert k_pages.stride() == v_pages.stride() and k_pages.stride(-1) == 1
+        comem_prefill_attn_paged(self.plan, q.data_ptr(), q_start.data_ptr(), q_lens.data_ptr(), int(max_q_len),
+                                 k_pages.data_ptr(), v_pages.data_ptr(), k_pages.stride(0), k_pages.stride(1),
+                                 k_pages.stride(2), k_pages.shape[1], k_pages.shape[0], block_table.data_ptr(),
+                                 block_table.shape[1], ctx_lens.data_ptr(), ctx_lens.shape[0], int(max_ctx_len),
+                                 out.data_ptr(), None if lse is None else lse.data_ptr(), self._stream(stream))
         return out, lse

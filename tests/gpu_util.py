@@ -94,3 +94,80 @@ def check(out, lse, ref_out, ref_lse, dtype, what=""):
         lim = (TOL_F32_ABS if dtype == "f32" else TOL_DIAG) * np.maximum(1.0, np.abs(ref_lse[~inf]))
         assert np.all(lerr <= lim), f"{what}: lse max err {lerr.max(initial=0):.3e}"
     return float(err.max(initial=0.0))
+
+
+# ------------------------------------------------------------------ prefill
+
+PREFILL_P_ROUNDING = 2.0 ** -15  # relative error of a probability split into two bf16 for the matrix cores
+
+
+class DevicePrefill:
+    """Device copies of a drawn prefill workload: the cache side plus the packed new-token queries."""
+
+    def __init__(self, pw, device="cuda:0"):
+        import torch
+
+        self.pw = pw
+        self.kv = DeviceWorkload(pw.kv, device)
+        s = pw.kv.spec
+        self.q = to_torch(pw.q, s.dtype, device)
+        self.q_start = torch.from_numpy(pw.q_start.astype(np.int64)).to(device)
+        self.q_lens = torch.from_numpy(pw.q_lens.astype(np.int32)).to(device)
+        self.max_q_len = int(pw.q_lens.max(initial=0))
+
+
+def run_prefill(dp: DevicePrefill, op, out=None, want_lse=True):
+    """One prefill call through the C ABI; returns (out, lse) as numpy float32."""
+    import torch
+
+    s = dp.pw.kv.spec
+    total = dp.q.shape[0]
+    lse = torch.full((total, s.num_q_heads), float("nan"), dtype=torch.float32, device=dp.q.device) \
+        if want_lse else None
+    kv = dp.kv
+    if s.layout == "paged":
+        out, lse = op.prefill_paged(dp.q, dp.q_start, dp.q_lens, dp.max_q_len, kv.k, kv.v, kv.block_table,
+                                    kv.ctx_lens, s.max_ctx_len, out=out, lse=lse)
+    else:
+        out, lse = op.prefill(dp.q, dp.q_start, dp.q_lens, dp.max_q_len, kv.k, kv.v, kv.seq_start, kv.ctx_lens,
+                              s.max_ctx_len, out=out, lse=lse)
+    torch.cuda.synchronize()
+    return out.cpu().numpy(), (None if lse is None else lse.cpu().numpy())
+
+
+def abs_values(pw):
+    """The same prefill workload with |V| in place of V (bf16: sign bit cleared), for error bounds."""
+    import dataclasses
+
+    kv = pw.kv
+    if kv.spec.dtype != "bf16":
+        raise ValueError("bf16 only")
+    if kv.spec.layout == "paged":
+        kv2 = dataclasses.replace(kv, v_pages=kv.v_pages & np.uint16(0x7FFF))
+    else:
+        kv2 = dataclasses.replace(kv, v=kv.v & np.uint16(0x7FFF))
+    return dataclasses.replace(pw, kv=kv2)
+
+
+def check_prefill(out, lse, ref_out, ref_lse, ref_abs, what=""):
+    """The official bf16 gate, plus the bound that the split probabilities imply: every element within
+    2 * 2^-15 * sum_t w_t |v_t| (ref_abs, half of it for fp32 accumulation) + 1e-5 |ref| + 1e-6.
+    Returns max |err|."""
+    out = np.asarray(out, dtype=np.float64)
+    ref_out = np.asarray(ref_out, dtype=np.float64)
+    assert out.shape == ref_out.shape, what
+    assert np.all(np.isfinite(out)), f"{what}: non-finite output"
+    err = np.abs(out - ref_out)
+    bad = err > TOL_BF16_ABS + TOL_BF16_REL * np.abs(ref_out)
+    assert not bad.any(), f"{what}: {bad.sum()} elements outside 2e-3 + 1e-2|ref| (max {err.max():.3e})"
+    bound = 2 * PREFILL_P_ROUNDING * np.asarray(ref_abs, dtype=np.float64) + 1e-5 * np.abs(ref_out) + 1e-6
+    over = err > bound
+    assert not over.any(), (f"{what}: {over.sum()} elements beyond the split-probability bound "
+                            f"(worst ratio {(err / bound).max():.3f})")
+    if lse is not None:
+        lse = np.asarray(lse, dtype=np.float64)
+        ref_lse = np.asarray(ref_lse, dtype=np.float64)
+        assert np.all(np.isfinite(lse)), f"{what}: non-finite lse"
+        lerr = np.abs(lse - ref_lse)
+        assert np.all(lerr <= 2e-5 * np.maximum(1.0, np.abs(ref_lse))), f"{what}: lse max err {lerr.max():.3e}"
+    return float(err.max(initial=0.0))

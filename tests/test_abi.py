@@ -14,15 +14,17 @@ import pytest
 from paper_2605_30842_amd import binding as B
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
-HEADER = os.path.join(ROOT, "include", "comem_decode_attn.h")
+HEADERS = [os.path.join(ROOT, "include", h) for h in ("comem_decode_attn.h", "comem_prefill_attn.h")]
 
 A = 1 << 20  # a 256-byte aligned fake device address (never dereferenced)
 
 
 def _declared_functions():
-    text = open(HEADER).read()
-    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
-    return sorted(set(re.findall(r"\b(comem_[a-z_]+)\s*\(", text)))
+    names = set()
+    for header in HEADERS:
+        text = re.sub(r"/\*.*?\*/", "", open(header).read(), flags=re.S)
+        names |= set(re.findall(r"\b(comem_[a-z_]+)\s*\(", text))
+    return sorted(names)
 
 
 def test_header_declares_what_the_binding_expects():
@@ -288,5 +290,70 @@ def test_auto_plan_fits_init_workspace(batch, L):
                 assert chunk % 32 == 0 and splits == -(-l // chunk)
                 chunk2, _ = B.comem_decode_attn_plan_splits(p, b, l, 1 << 40)
                 assert chunk2 == chunk, "init workspace forced a coarser plan"
+    finally:
+        B.comem_decode_attn_destroy(p)
+
+
+def _prefill_args(plan, **kw):
+    args = dict(plan=plan, q=A, q_start=A, q_lens=A, max_q_len=512, k=A, v=A, stride_token=8 * 128, stride_head=128,
+                seq_start=A, ctx_lens=A, batch=2, max_ctx_len=4096, out=A, lse=A, stream=None)
+    args.update(kw)
+    return args
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(), B.ERR_NO_DEVICE),
+    (dict(batch=0, q=None), B.OK),
+    (dict(max_q_len=0), B.OK),
+    (dict(batch=-1), B.ERR_INVALID_SHAPE),
+    (dict(batch=5), B.ERR_INVALID_SHAPE),
+    (dict(max_ctx_len=4097), B.ERR_INVALID_SHAPE),
+    (dict(max_q_len=-1), B.ERR_INVALID_SHAPE),
+    (dict(max_q_len=4097), B.ERR_INVALID_SHAPE),
+    (dict(q=None), B.ERR_NULL_POINTER),
+    (dict(q_start=None), B.ERR_NULL_POINTER),
+    (dict(q_lens=None), B.ERR_NULL_POINTER),
+    (dict(k=None), B.ERR_NULL_POINTER),
+    (dict(seq_start=None), B.ERR_NULL_POINTER),
+    (dict(ctx_lens=None), B.ERR_NULL_POINTER),
+    (dict(out=None), B.ERR_NULL_POINTER),
+    (dict(lse=None), B.ERR_NO_DEVICE),
+    (dict(stride_token=0), B.ERR_INVALID_SHAPE),
+    (dict(stride_token=8 * 128 + 4), B.ERR_MISALIGNED),
+    (dict(q=A + 8), B.ERR_MISALIGNED),
+    (dict(out=A + 4), B.ERR_MISALIGNED),
+    (dict(q_start=A + 4), B.ERR_MISALIGNED),
+    (dict(q_lens=A + 2), B.ERR_MISALIGNED),
+    (dict(seq_start=A + 4), B.ERR_MISALIGNED),
+])
+def test_prefill_validation(plan, kw, status):
+    p, _ = plan
+    assert B.load_library().comem_prefill_attn(*_prefill_args(p, **kw).values()) == status
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(), B.ERR_NO_DEVICE),
+    (dict(block_table=None), B.ERR_NULL_POINTER),
+    (dict(page_size=24), B.ERR_INVALID_SHAPE),
+    (dict(num_pages=0), B.ERR_INVALID_SHAPE),
+    (dict(max_pages=255), B.ERR_INVALID_SHAPE),
+    (dict(block_table=A + 2), B.ERR_MISALIGNED),
+    (dict(q_lens=None), B.ERR_NULL_POINTER),
+    (dict(batch=0, block_table=None), B.OK),
+])
+def test_prefill_paged_validation(plan, kw, status):
+    p, _ = plan
+    args = dict(plan=p, q=A, q_start=A, q_lens=A, max_q_len=512, k=A, v=A, stride_page=16 * 8 * 128,
+                stride_token=8 * 128, stride_head=128, page_size=16, num_pages=100, block_table=A, max_pages=256,
+                ctx_lens=A, batch=2, max_ctx_len=4096, out=A, lse=A, stream=None)
+    args.update(kw)
+    assert B.load_library().comem_prefill_attn_paged(*args.values()) == status
+    assert B.load_library().comem_prefill_attn_paged(*dict(args, plan=None).values()) == B.ERR_BAD_HANDLE
+
+
+def test_prefill_needs_bf16():
+    p, _ = B.comem_decode_attn_init(_cfg(dtype=B.F32), B.NO_DEVICE)
+    try:
+        assert B.load_library().comem_prefill_attn(*_prefill_args(p).values()) == B.ERR_UNSUPPORTED
     finally:
         B.comem_decode_attn_destroy(p)
