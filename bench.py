@@ -31,6 +31,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 PEAK_HBM_GBPS = 8000.0
+PEAK_BF16_TFLOPS = 2500.0  # MI355X dense bf16 matrix-core peak
 PROFILES = os.path.join(ROOT, "profiles")
 KERNEL_SOURCES = ["paper_2605_30842_amd/csrc/api.cpp", "paper_2605_30842_amd/csrc/attn_common.h",
                   "paper_2605_30842_amd/csrc/kernel_mfma.hip", "paper_2605_30842_amd/csrc/kernel_valu.hip"]
@@ -58,6 +59,8 @@ def _args():
                     help="instead of attention, time the streaming-read or copy probe kernel")
     ap.add_argument("--probe-bytes", type=int, default=4 << 30)
     ap.add_argument("--probe-blocks", type=int, default=4096)
+    ap.add_argument("--prefill", type=int, default=0,
+                    help="instead of decode, time the prefill-attention call on named prefill workload N (1..3)")
     ap.add_argument("--summarize", metavar="DIR", default=None,
                     help="write profiles/ summaries from rocprofv3 outputs under DIR (layout in summarize())")
     return ap.parse_args()
@@ -254,6 +257,106 @@ def _cpu_baseline(w, budget_s):
             "host_cpus": len(os.sched_getaffinity(0))}
 
 
+def _prefill_cpu_baseline(pw, budget_s):
+    """Time the fp64 prefill oracle on whole rows (new token, query head) of the same workload."""
+    import oracle.prefill_attention as pa
+
+    try:
+        from threadpoolctl import threadpool_info
+
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+    except Exception:  # noqa: BLE001
+        threads = 1
+    s = pw.kv.spec
+    b = 0
+    M = int(pw.q_lens[b])
+    L = int(pw.kv.ctx_lens[b])
+    rows = [(b, M - 1 - i, h) for i in range(min(M, 8)) for h in range(s.num_q_heads)]
+    flops = sum(4 * s.head_dim * (L - M + i + 1) for (_, i, _) in rows)
+    t0 = time.perf_counter()
+    pa.prefill_attention_rows(pw, rows)
+    one = time.perf_counter() - t0
+    reps = max(1, int(budget_s / max(one, 1e-3)))
+    t0 = time.perf_counter()
+    for _ in range(reps):
+        pa.prefill_attention_rows(pw, rows)
+    dt = (time.perf_counter() - t0) / reps
+    return {"value": round(flops / dt / 1e12, 6), "unit": "TFLOP/s", "cores": threads, "kind": "oracle",
+            "sample": f"{reps} oracle calls over the last {min(M, 8)} new tokens x {s.num_q_heads} heads of "
+                      f"sequence 0 ({L} cached tokens), float64 numpy",
+            "seconds_per_call": round(dt, 4), "host_cpus": len(os.sched_getaffinity(0))}
+
+
+def _prefill(a):
+    """Prefill attention (cached prefix + causal new tokens) on a named prefill workload."""
+    import torch
+
+    from paper_2605_30842_amd import binding
+    from paper_2605_30842_amd.binding import DecodeAttention
+    from workloads.synth import PREFILL_WORKLOADS, generate_prefill
+
+    binding.load_library()
+    pspec = PREFILL_WORKLOADS[a.prefill]
+    pw = generate_prefill(pspec)
+    s = pw.kv.spec
+    dev = torch.device("cuda:0")
+
+    def dev_t(x):
+        return torch.from_numpy(np.ascontiguousarray(x).view(np.int16)).view(torch.bfloat16).to(dev)
+
+    q = dev_t(pw.q)
+    q_start = torch.from_numpy(pw.q_start.astype(np.int64)).to(dev)
+    q_lens = torch.from_numpy(pw.q_lens.astype(np.int32)).to(dev)
+    ctx = torch.from_numpy(pw.kv.ctx_lens.astype(np.int32)).to(dev)
+    paged = s.layout == "paged"
+    k = dev_t(pw.kv.k_pages if paged else pw.kv.k)
+    v = dev_t(pw.kv.v_pages if paged else pw.kv.v)
+    bt = torch.from_numpy(pw.kv.block_table.astype(np.int32)).to(dev) if paged else None
+    ss = None if paged else torch.from_numpy(pw.kv.seq_start.astype(np.int64)).to(dev)
+    op = DecodeAttention(s.num_q_heads, s.num_kv_heads, s.head_dim, s.dtype, float(s.scale), s.batch,
+                         s.max_ctx_len)
+    out = torch.empty(q.shape, dtype=torch.float32, device=dev)
+    lse = torch.empty(q.shape[:2], dtype=torch.float32, device=dev)
+    max_q = int(pw.q_lens.max())
+
+    def step(stream):
+        if paged:
+            op.prefill_paged(q, q_start, q_lens, max_q, k, v, bt, ctx, s.max_ctx_len, out=out, lse=lse, stream=stream)
+        else:
+            op.prefill(q, q_start, q_lens, max_q, k, v, ss, ctx, s.max_ctx_len, out=out, lse=lse, stream=stream)
+
+    stream = torch.cuda.current_stream()
+    for _ in range(a.warmup):
+        step(stream)
+    torch.cuda.synchronize()
+    eager_out = out.clone()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(a.steps):
+        step(stream)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    eager_ms = e0.elapsed_time(e1) / a.steps
+    assert torch.equal(out, eager_out), "repeated prefill calls differ"
+    assert torch.isfinite(out).all().item()
+    flops = pw.flops
+    tflops = flops / (eager_ms * 1e-3) / 1e12
+    cpu = _prefill_cpu_baseline(pw, a.cpu_seconds) if a.cpu_seconds > 0 else None
+    print(json.dumps({
+        "metric": "prefill-attention TFLOP/s (algorithmic: 4 * head_dim * query heads * visible pairs)",
+        "value": round(tflops, 3), "unit": "TFLOP/s", "n_gpus": 1, "steps": a.steps, "warmup": a.warmup,
+        "ms_per_step": round(eager_ms, 6), "us_per_step": round(eager_ms * 1e3, 3), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": pspec.name, "batch": s.batch, "num_q_heads": s.num_q_heads,
+                   "num_kv_heads": s.num_kv_heads, "head_dim": s.head_dim, "layout": s.layout,
+                   "page_size": s.page_size, "new_tokens": int(pw.q_lens.sum()),
+                   "cached_tokens": int(pw.kv.ctx_lens.sum()), "flops_per_step": flops, "timing": "eager"},
+        "roofline": {"bound": "mfma", "achieved": round(tflops, 3), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                     "frac": round(tflops / PEAK_BF16_TFLOPS, 4), "traffic": None},
+        "cpu_baseline": cpu,
+    }), flush=True)
+
+
 def main():
     a = _args()
     if a.gpus != 1:
@@ -265,6 +368,9 @@ def main():
         return
     if a.summarize:
         summarize(a)
+        return
+    if a.prefill:
+        _prefill(a)
         return
     import torch
 

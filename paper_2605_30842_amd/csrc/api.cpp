@@ -391,7 +391,7 @@ comem_status prepare_prefill(const comem_decode_attn_plan& p, const void* q, con
 
 comem_status launch_prefill(const comem_decode_attn_plan& p, const comem::PrefillParams& a, bool paged,
                             int32_t batch, int32_t max_q_len, void* stream) {
-  comem::PrefillKernelFn fn = comem::select_prefill_kernel(p.cfg.head_dim, paged);
+  comem::PrefillKernelFn fn = comem::select_prefill_kernel(p.cfg.head_dim, paged ? a.page_mask + 1 : 0);
   if (fn == nullptr) return COMEM_ERR_UNSUPPORTED;
   const int64_t blocks = ceil_div(max_q_len, a.tokens_per_block);
   comem::PrefillParams args = a;

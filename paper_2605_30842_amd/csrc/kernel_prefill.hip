@@ -30,19 +30,30 @@
 //     e of k-step (block sb, step s2) is register 8 s2 + e, i.e. key
 //     32 sb + 16 s2 + 8 (e / 4) + 4 h + e % 4. The reduction index of an MFMA
 //     is a dummy index, so A = V^T uses the same key for the same (half,
-//     element): lane (i, h) reads those 8 V rows at head_dim NT i .. NT i +
-//     NT - 1 (NT = D / 32) and n-tile n takes entry NT i + n of each, packed
-//     in pairs with v_perm. Output row i of n-tile n is head_dim NT i + n.
+//     element); row i of n-tile n is head_dim 32 n + i. That operand holds 8
+//     keys at one head_dim entry per lane, a transpose of how V is stored; the
+//     LDS transpose read (ds_read_b64_tr_b16) produces it directly: within a
+//     group of 16 lanes, lane 4a + c receives element c of the 4-element
+//     vectors addressed by lanes a, a + 4, a + 8, a + 12 (checked on the
+//     device). So lane k of a group addresses key (k / 4) of the step at
+//     head_dim 4 (k % 4) onward, and two reads give the 8 keys.
 // P is split as P = P_hi + P_lo, both bf16 (the high half truncated, the
 // exact remainder rounded to nearest even), and both halves are multiplied,
 // so each weight keeps about 16 significant bits: an output is off by at
 // most about 2^-15 sum_t w_t |v_t| plus fp32 rounding.
 //
+// The running maximum moves lazily: it is raised only when a row's new
+// maximum exceeds it by more than 2^8 in probability, so the accumulators are
+// rescaled rarely and every probability stays below 2^8.
+//
 // K and V tiles go global -> registers -> LDS, one tile ahead of the compute,
-// into two LDS buffers; 16-byte chunks are XOR-swizzled by row so that the
-// K reads of 32 rows and the V reads of whole rows are free of bank
-// conflicts. Paged caches look their block-table entries up one tile ahead
-// of the data loads.
+// into two LDS buffers. Global loads use buffer descriptors whose base and
+// size are uniform per tile (or per 16-row group of a page), so addresses are
+// scalar arithmetic and rows past the keys a block needs read as zero. In
+// LDS, 16-byte chunk c of row r sits at chunk c ^ f(r), with f chosen so that
+// the K reads (one chunk of 8 or 16 consecutive rows), the V transpose reads
+// (4 chunks of 4 consecutive rows) and the stores are all free of bank
+// conflicts. Paged caches look their block-table entries up one tile ahead.
 #include "attn_common.h"
 #include "prefill.h"
 
@@ -50,27 +61,40 @@ namespace comem {
 namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
-typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
+
+constexpr float kLazyMax = 8.f;  // log2 of the largest probability the lazy maximum allows
 
 template <int D>
 struct PrefillSmem {
   static constexpr int kRowBytes = D * 2;
   static constexpr int kTileBytes = kPrefillTileKeys * kRowBytes;
-  char k[2][kTileBytes];
-  char v[2][kTileBytes];
+  static constexpr int kBufBytes = 2 * kTileBytes;  // K then V of one buffer
+  char buf[2][2][kTileBytes];                       // [buffer][K, V]
 };
 
-// Byte offset of 16-byte chunk c of tile row r in LDS.
+// Chunk swizzle of a row (depends on its low 4 bits only).
 template <int D>
-__device__ inline int swizzled(int r, int c) {
-  constexpr int CH = D / 8;
-  return r * (D * 2) + ((c ^ (r & (CH - 1))) << 4);
+__device__ inline int swizzle(int r) {
+  if constexpr (D == 128) return ((r & 3) << 2) | ((r >> 2) & 3);
+  return (((r >> 1) & 1) << 2) | ((r >> 2) & 3);
 }
 
+// Byte offset of logical 16-byte chunk c of tile row r.
+template <int D>
+__device__ inline int lds_offset(int r, int c) {
+  return r * (D * 2) + ((c ^ swizzle<D>(r)) << 4);
+}
+
+enum class PLayout { kContig, kPaged, kPagedFine };
+
 // One thread's share of a K/V tile: chunk c of rows row0 + RSTEP u.
-template <int D, bool PAGED>
+template <int D, PLayout LAYOUT>
 struct TileLoader {
   static constexpr int CH = D / 8;                    // 16-byte chunks per row
   static constexpr int RSTEP = kPrefillThreads / CH;  // rows between a thread's chunks
@@ -81,68 +105,78 @@ struct TileLoader {
   int64_t stride_token;
   int64_t stride_page;
   int page_shift, page_mask;
-  int kend;  // keys [0, kend) are read; later rows repeat key kend - 1
+  int kend;  // keys [0, kend) are read; later rows read as zero (or repeat key kend - 1)
   int c, row0;
+  uint32_t voff;  // row0 * stride_token + 16 c
   u32x4 kreg[NU], vreg[NU];
-  int32_t page[NU];
+  int32_t page[NU];  // kPaged: one entry per group of RSTEP rows; kPagedFine: per row
+
+  // Buffer descriptor over `rows` rows from `base`; never more than 4 GiB.
+  __device__ __amdgpu_buffer_rsrc_t rsrc(const char* base, int rows) const {
+    const int64_t bytes = static_cast<int64_t>(rows) * stride_token;
+    const uint32_t n = bytes > 0xffffffffll ? 0xffffffffu : static_cast<uint32_t>(bytes);
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<char*>(base), 0, static_cast<int>(n), kBufferConfig);
+  }
 
   __device__ int key(int t0, int u) const { return min(t0 + row0 + u * RSTEP, kend - 1); }
 
   __device__ void fetch_pages(int t0) {
-    if constexpr (PAGED) {
+    if constexpr (LAYOUT == PLayout::kPaged) {
+#pragma unroll
+      for (int u = 0; u < NU; ++u) {
+        const int g0 = t0 + u * RSTEP;
+        page[u] = g0 < kend ? bt_row[g0 >> page_shift] : 0;
+      }
+    } else if constexpr (LAYOUT == PLayout::kPagedFine) {
 #pragma unroll
       for (int u = 0; u < NU; ++u) page[u] = bt_row[key(t0, u) >> page_shift];
     }
   }
 
   __device__ void load(int t0) {
+    if constexpr (LAYOUT == PLayout::kContig) {
+      const int64_t base = static_cast<int64_t>(t0) * stride_token;
+      const int rows = min(kend - t0, kPrefillTileKeys);
+      const __amdgpu_buffer_rsrc_t rk = rsrc(kbase + base, rows), rv = rsrc(vbase + base, rows);
 #pragma unroll
-    for (int u = 0; u < NU; ++u) {
-      const int t = key(t0, u);
-      int64_t off;
-      if constexpr (PAGED) {
-        off = static_cast<int64_t>(page[u]) * stride_page + static_cast<int64_t>(t & page_mask) * stride_token;
-      } else {
-        off = static_cast<int64_t>(t) * stride_token;
+      for (int u = 0; u < NU; ++u) {
+        const int so = static_cast<int>(static_cast<uint32_t>(u * RSTEP * stride_token));
+        kreg[u] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rk, voff, so, 0));
+        vreg[u] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rv, voff, so, 0));
       }
-      off += c * 16;
-      kreg[u] = *reinterpret_cast<const u32x4*>(kbase + off);
-      vreg[u] = *reinterpret_cast<const u32x4*>(vbase + off);
+    } else if constexpr (LAYOUT == PLayout::kPaged) {
+      // A group of RSTEP rows lies in one page (page_size >= RSTEP).
+#pragma unroll
+      for (int u = 0; u < NU; ++u) {
+        const int g0 = t0 + u * RSTEP;
+        const int rows = max(0, min(kend - g0, RSTEP));
+        const int64_t base =
+            static_cast<int64_t>(page[u]) * stride_page + static_cast<int64_t>(g0 & page_mask) * stride_token;
+        const __amdgpu_buffer_rsrc_t rk = rsrc(kbase + base, rows), rv = rsrc(vbase + base, rows);
+        kreg[u] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rk, voff, 0, 0));
+        vreg[u] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rv, voff, 0, 0));
+      }
+    } else {
+#pragma unroll
+      for (int u = 0; u < NU; ++u) {
+        const int t = key(t0, u);
+        const int64_t off = static_cast<int64_t>(page[u]) * stride_page +
+                            static_cast<int64_t>(t & page_mask) * stride_token + c * 16;
+        kreg[u] = *reinterpret_cast<const u32x4*>(kbase + off);
+        vreg[u] = *reinterpret_cast<const u32x4*>(vbase + off);
+      }
     }
   }
 
-  __device__ void store(PrefillSmem<D>& sm, int buf) const {
+  __device__ void store(PrefillSmem<D>& sm, int b) const {
 #pragma unroll
     for (int u = 0; u < NU; ++u) {
-      const int off = swizzled<D>(row0 + u * RSTEP, c);
-      *reinterpret_cast<u32x4*>(sm.k[buf] + off) = kreg[u];
-      *reinterpret_cast<u32x4*>(sm.v[buf] + off) = vreg[u];
+      const int off = lds_offset<D>(row0 + u * RSTEP, c);
+      *reinterpret_cast<u32x4*>(sm.buf[b][0] + off) = kreg[u];
+      *reinterpret_cast<u32x4*>(sm.buf[b][1] + off) = vreg[u];
     }
   }
 };
-
-// NT consecutive bf16 of a V row, as read for the V^T operand.
-template <int D>
-struct VPiece;
-template <>
-struct VPiece<128> {
-  u32x2 w;
-  __device__ uint32_t word(int n) const { return w[n >> 1]; }
-  __device__ void read(const char* tile, int r, int j) {
-    w = *reinterpret_cast<const u32x2*>(tile + swizzled<128>(r, j >> 1) + ((j & 1) << 3));
-  }
-};
-template <>
-struct VPiece<64> {
-  uint32_t w;
-  __device__ uint32_t word(int) const { return w; }
-  __device__ void read(const char* tile, int r, int j) {
-    w = *reinterpret_cast<const uint32_t*>(tile + swizzled<64>(r, j >> 2) + ((j & 3) << 2));
-  }
-};
-
-typedef float f32x2 __attribute__((ext_vector_type(2)));
-typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 
 // p0, p1 -> (hi, lo) bf16 pairs with p = hi + lo to about 2^-16 relative:
 // hi keeps the upper 16 bits of each value, lo is the exact fp32 remainder
@@ -154,26 +188,50 @@ __device__ inline void split_bf16(float p0, float p1, uint32_t& hi, uint32_t& lo
   lo = __builtin_bit_cast(uint32_t, __builtin_convertvector(r, bf16x2));
 }
 
+// Per-lane LDS offsets, fixed for the whole kernel.
+template <int D>
+struct LaneOffsets {
+  int k;     // K reads: row j, logical chunk h, with the row's swizzle (XOR 32 ks for step ks)
+  int v[2];  // V transpose reads, step half c2: key 8 c2 + 4 h + k / 4 of the step, head_dim 4 (k % 4)
+             // + 16 (group parity) of n-tile 0 (XOR 64 n for n-tile n)
+};
+
+template <int D>
+__device__ inline LaneOffsets<D> lane_offsets(int lane) {
+  LaneOffsets<D> o;
+  const int j = lane & 31, h = lane >> 5;
+  o.k = j * (D * 2) + ((h ^ swizzle<D>(j)) << 4);
+  const int k16 = lane & 15, gpar = (lane >> 4) & 1;
+  const int hb = 2 * (k16 & 3) * 4;  // byte offset of head_dim 4 (k % 4) within 32 head_dim entries
+#pragma unroll
+  for (int c2 = 0; c2 < 2; ++c2) {
+    const int r = 8 * c2 + 4 * h + (k16 >> 2);
+    const int byte = 32 * gpar + hb;  // within the first 64 bytes (n-tile 0)
+    o.v[c2] = r * (D * 2) + (((byte >> 4) ^ swizzle<D>(r)) << 4) + (byte & 15);
+  }
+  return o;
+}
+
 // One 64-key tile for the 32 rows of a wave. `limit` is the last key the
 // lane's row may see; MASKED is false when every key of the tile is visible
 // to every row of the workgroup.
 template <int D, bool MASKED>
-__device__ inline void compute_tile(const PrefillSmem<D>& sm, int buf, int t0, int limit, int j,
-                                    int h, const bf16x8 (&qop)[D / 16], float scale_log2, float& m_run,
-                                    float& l_run, f32x16 (&acc)[D / 32]) {
+__device__ inline void compute_tile(const PrefillSmem<D>& sm, int b, int t0, int limit, int h,
+                                    const LaneOffsets<D>& lo, const bf16x8 (&qop)[D / 16], float scale_log2,
+                                    float& m_run, float& l_run, f32x16 (&acc)[D / 32]) {
   constexpr int KS = D / 16;
   constexpr int NT = D / 32;
-  const char* kt = sm.k[buf];
-  const char* vt = sm.v[buf];
+  constexpr int RB = D * 2;
+  const char* kt = sm.buf[b][0];
+  const char* vt = sm.buf[b][1];
 
-  f32x16 s[2];
+  f32x16 s[2] = {f32x16{}, f32x16{}};
 #pragma unroll
-  for (int sb = 0; sb < 2; ++sb) {
-    s[sb] = f32x16{};
-    const int r = 32 * sb + j;
+  for (int ks = 0; ks < KS; ++ks) {
+    const int off = lo.k ^ (32 * ks);
 #pragma unroll
-    for (int ks = 0; ks < KS; ++ks) {
-      const bf16x8 a = *reinterpret_cast<const bf16x8*>(kt + swizzled<D>(r, 2 * ks + h));
+    for (int sb = 0; sb < 2; ++sb) {
+      const bf16x8 a = *reinterpret_cast<const bf16x8*>(kt + off + 32 * sb * RB);
       s[sb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qop[ks], s[sb], 0, 0, 0);
     }
   }
@@ -192,15 +250,18 @@ __device__ inline void compute_tile(const PrefillSmem<D>& sm, int buf, int t0, i
       mt = fmaxf(mt, s[sb][r]);
     }
   mt = fmaxf(mt, __shfl_xor(mt, 32));
-  // The first tile holds key 0, visible to every row, so m_new is finite.
-  const float m_new = fmaxf(m_run, mt);
-  const float alpha = fast_exp2((m_run - m_new) * scale_log2);
-  if (__builtin_amdgcn_ballot_w64(alpha != 1.f) != 0) {
+  // Lazy maximum: move it only when some row would see a probability above
+  // 2^kLazyMax. The first tile holds key 0, visible to every row, so the
+  // maximum is finite from then on.
+  if (__builtin_amdgcn_ballot_w64((mt - m_run) * scale_log2 > kLazyMax) != 0) {
+    const float m_new = fmaxf(m_run, mt);
+    const float alpha = fast_exp2((m_run - m_new) * scale_log2);
 #pragma unroll
     for (int n = 0; n < NT; ++n) acc[n] *= alpha;
+    l_run *= alpha;
+    m_run = m_new;
   }
-  m_run = m_new;
-  const float mb = m_new * scale_log2;
+  const float mb = m_run * scale_log2;
 
   float psum = 0.f;
 #pragma unroll
@@ -217,30 +278,29 @@ __device__ inline void compute_tile(const PrefillSmem<D>& sm, int buf, int t0, i
       }
       const bf16x8 pb_hi = __builtin_bit_cast(bf16x8, u32x4{ph[0], ph[1], ph[2], ph[3]});
       const bf16x8 pb_lo = __builtin_bit_cast(bf16x8, u32x4{pl[0], pl[1], pl[2], pl[3]});
-      VPiece<D> vr[8];
-#pragma unroll
-      for (int e = 0; e < 8; ++e) vr[e].read(vt, 32 * sb + 16 * s2 + 8 * (e >> 2) + 4 * h + (e & 3), j);
+      const int step = (32 * sb + 16 * s2) * RB;
 #pragma unroll
       for (int n = 0; n < NT; ++n) {
-        const uint32_t sel = (n & 1) ? 0x07060302u : 0x05040100u;
-        u32x4 va;
-#pragma unroll
-        for (int e = 0; e < 8; e += 2) va[e >> 1] = __builtin_amdgcn_perm(vr[e + 1].word(n), vr[e].word(n), sel);
-        const bf16x8 vop = __builtin_bit_cast(bf16x8, va);
+        const bf16x4 v0 = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
+            (lds_bf16x4*)(vt + step + (lo.v[0] ^ (64 * n))));
+        const bf16x4 v1 = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
+            (lds_bf16x4*)(vt + step + (lo.v[1] ^ (64 * n))));
+        const bf16x8 vop = __builtin_shufflevector(v0, v1, 0, 1, 2, 3, 4, 5, 6, 7);
         acc[n] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vop, pb_hi, acc[n], 0, 0, 0);
         acc[n] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vop, pb_lo, acc[n], 0, 0, 0);
       }
     }
-  l_run = l_run * alpha + psum;
+  l_run += psum;
 }
 
 // Grid: (query blocks, KV heads, sequences). Query blocks are taken in
 // reverse order so that, for causal attention, the blocks with the most keys
 // start first.
-template <int D, bool PAGED>
+template <int D, PLayout LAYOUT>
 __global__ __launch_bounds__(kPrefillThreads, 2) void prefill_mfma_kernel(const PrefillParams p) {
   constexpr int KS = D / 16;
   constexpr int NT = D / 32;
+  constexpr bool PAGED = LAYOUT != PLayout::kContig;
   __shared__ PrefillSmem<D> sm;
   const int b = blockIdx.z, hk = blockIdx.y;
   const int qb = gridDim.x - 1 - blockIdx.x;
@@ -269,7 +329,8 @@ __global__ __launch_bounds__(kPrefillThreads, 2) void prefill_mfma_kernel(const 
   const int qh = hk * p.group + g;
   const int limit = prefix + ic;
 
-  TileLoader<D, PAGED> ld;
+  using Loader = TileLoader<D, LAYOUT>;
+  Loader ld;
   ld.kbase = p.k + hk * p.stride_head + seq0 * p.stride_token;
   ld.vbase = p.v + hk * p.stride_head + seq0 * p.stride_token;
   ld.bt_row = PAGED ? p.block_table + static_cast<int64_t>(b) * p.max_pages : nullptr;
@@ -278,8 +339,9 @@ __global__ __launch_bounds__(kPrefillThreads, 2) void prefill_mfma_kernel(const 
   ld.page_shift = p.page_shift;
   ld.page_mask = p.page_mask;
   ld.kend = kend;
-  ld.c = threadIdx.x % TileLoader<D, PAGED>::CH;
-  ld.row0 = threadIdx.x / TileLoader<D, PAGED>::CH;
+  ld.c = threadIdx.x % Loader::CH;
+  ld.row0 = threadIdx.x / Loader::CH;
+  ld.voff = static_cast<uint32_t>(ld.row0 * p.stride_token + 16 * ld.c);
 
   ld.fetch_pages(0);
   ld.load(0);
@@ -292,6 +354,7 @@ __global__ __launch_bounds__(kPrefillThreads, 2) void prefill_mfma_kernel(const 
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) qop[ks] = *reinterpret_cast<const bf16x8*>(qrow + 32 * ks + 16 * h);
   }
+  const LaneOffsets<D> lo = lane_offsets<D>(lane);
   f32x16 acc[NT];
 #pragma unroll
   for (int n = 0; n < NT; ++n) acc[n] = f32x16{};
@@ -307,7 +370,7 @@ __global__ __launch_bounds__(kPrefillThreads, 2) void prefill_mfma_kernel(const 
       ld.load(kPrefillTileKeys * (t + 1));
       if (t + 2 < ntiles) ld.fetch_pages(kPrefillTileKeys * (t + 2));
     }
-    compute_tile<D, false>(sm, t & 1, kPrefillTileKeys * t, limit, j, h, qop, p.scale_log2, m_run, l_run, acc);
+    compute_tile<D, false>(sm, t & 1, kPrefillTileKeys * t, limit, h, lo, qop, p.scale_log2, m_run, l_run, acc);
     if (more) ld.store(sm, (t + 1) & 1);
     __syncthreads();
   }
@@ -317,7 +380,7 @@ __global__ __launch_bounds__(kPrefillThreads, 2) void prefill_mfma_kernel(const 
       ld.load(kPrefillTileKeys * (t + 1));
       if (t + 2 < ntiles) ld.fetch_pages(kPrefillTileKeys * (t + 2));
     }
-    compute_tile<D, true>(sm, t & 1, kPrefillTileKeys * t, limit, j, h, qop, p.scale_log2, m_run, l_run, acc);
+    compute_tile<D, true>(sm, t & 1, kPrefillTileKeys * t, limit, h, lo, qop, p.scale_log2, m_run, l_run, acc);
     if (more) ld.store(sm, (t + 1) & 1);
     __syncthreads();
   }
@@ -327,24 +390,30 @@ __global__ __launch_bounds__(kPrefillThreads, 2) void prefill_mfma_kernel(const 
   const float inv = 1.f / l_run;
   const int64_t orow = (qs + i) * p.num_q_heads + qh;
   float* o = p.out + orow * D;
+  // acc[n] register r holds head_dim 32 n + 8 (r / 4) + 4 h + r % 4.
 #pragma unroll
-  for (int r = 0; r < 16; ++r) {
-    const int d0 = NT * (8 * (r >> 2) + 4 * h + (r & 3));
-    if constexpr (NT == 4) {
-      *reinterpret_cast<float4*>(o + d0) =
-          make_float4(acc[0][r] * inv, acc[1][r] * inv, acc[2][r] * inv, acc[3][r] * inv);
-    } else {
-      *reinterpret_cast<float2*>(o + d0) = make_float2(acc[0][r] * inv, acc[1][r] * inv);
-    }
-  }
+  for (int n = 0; n < NT; ++n)
+#pragma unroll
+    for (int r4 = 0; r4 < 4; ++r4)
+      *reinterpret_cast<float4*>(o + 32 * n + 8 * r4 + 4 * h) =
+          make_float4(acc[n][4 * r4] * inv, acc[n][4 * r4 + 1] * inv, acc[n][4 * r4 + 2] * inv,
+                      acc[n][4 * r4 + 3] * inv);
   if (h == 0 && p.lse != nullptr) p.lse[orow] = (m_run * p.scale_log2 + log2f(l_run)) * kLn2;
 }
 
 }  // namespace
 
-PrefillKernelFn select_prefill_kernel(int head_dim, bool paged) {
-  if (head_dim == 128) return paged ? prefill_mfma_kernel<128, true> : prefill_mfma_kernel<128, false>;
-  if (head_dim == 64) return paged ? prefill_mfma_kernel<64, true> : prefill_mfma_kernel<64, false>;
+PrefillKernelFn select_prefill_kernel(int head_dim, int page_size) {
+  // page_size 0: contiguous cache. A paged cache takes the per-group path when
+  // a group of a thread's rows (kPrefillThreads / (head_dim / 8) rows) fits in a page.
+  if (head_dim == 128) {
+    if (page_size == 0) return prefill_mfma_kernel<128, PLayout::kContig>;
+    return page_size >= 16 ? prefill_mfma_kernel<128, PLayout::kPaged> : prefill_mfma_kernel<128, PLayout::kPagedFine>;
+  }
+  if (head_dim == 64) {
+    if (page_size == 0) return prefill_mfma_kernel<64, PLayout::kContig>;
+    return page_size >= 32 ? prefill_mfma_kernel<64, PLayout::kPaged> : prefill_mfma_kernel<64, PLayout::kPagedFine>;
+  }
   return nullptr;
 }
 

@@ -35,6 +35,7 @@ struct PrefillParams {
 };
 
 using PrefillKernelFn = void (*)(PrefillParams);
-PrefillKernelFn select_prefill_kernel(int head_dim, bool paged);
+// page_size 0 selects the contiguous-cache kernel.
+PrefillKernelFn select_prefill_kernel(int head_dim, int page_size);
 
 }  // namespace comem
