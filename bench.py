@@ -35,6 +35,8 @@ PEAK_BF16_TFLOPS = 2500.0  # MI355X dense bf16 matrix-core peak
 PROFILES = os.path.join(ROOT, "profiles")
 KERNEL_SOURCES = ["paper_2605_30842_amd/csrc/api.cpp", "paper_2605_30842_amd/csrc/attn_common.h",
                   "paper_2605_30842_amd/csrc/kernel_mfma.hip", "paper_2605_30842_amd/csrc/kernel_valu.hip"]
+PREFILL_SOURCES = ["paper_2605_30842_amd/csrc/api.cpp", "paper_2605_30842_amd/csrc/attn_common.h",
+                   "paper_2605_30842_amd/csrc/prefill.h", "paper_2605_30842_amd/csrc/kernel_prefill.hip"]
 COPY_CAL_BYTES = 256 << 20  # size of the copy used to calibrate FETCH_SIZE / WRITE_SIZE
 METRIC = "decode-attention effective HBM GB/s (% of peak) and µs/step at 32k-128k ctx"
 MALL_BYTES = 256 << 20
@@ -66,9 +68,9 @@ def _args():
     return ap.parse_args()
 
 
-def kernel_source_hash() -> str:
+def kernel_source_hash(sources=KERNEL_SOURCES) -> str:
     h = hashlib.sha256()
-    for rel in KERNEL_SOURCES:
+    for rel in sources:
         with open(os.path.join(ROOT, rel), "rb") as f:
             h.update(f.read())
     return h.hexdigest()[:16]
@@ -80,7 +82,7 @@ def _counter_medians(path):
     for f in glob.glob(os.path.join(path, "**", "*counter_collection.csv"), recursive=True):
         for r in csv.DictReader(open(f)):
             k = r["Kernel_Name"]
-            kind = "attn" if "decode_" in k else ("copy" if "copy_kernel" in k else None)
+            kind = "attn" if ("decode_" in k or "prefill_" in k) else ("copy" if "copy_kernel" in k else None)
             if kind:
                 vals.setdefault((kind, r["Counter_Name"]), []).append(float(r["Counter_Value"]))
     return {k: sorted(v)[len(v) // 2] for k, v in vals.items()}
@@ -90,7 +92,7 @@ def _short_kernel_name(full):
     """decode_mfma_queue_kernel<128, Layout 1> -> decode_mfma_queue_D128_paged (and similar)."""
     import re
 
-    m = re.search(r"(decode_\w+?)(?:_kernel)?<([^>]*)>", full)
+    m = re.search(r"((?:decode|prefill)_\w+?)(?:_kernel)?<([^>]*)>", full)
     if not m:
         return re.sub(r"\W+", "_", full.split("<")[0]).strip("_")[:60]
     base, args = m.group(1), m.group(2)
@@ -122,11 +124,12 @@ def summarize(a):
     """profiles/<kernel>_<workload>.md from the rocprofv3 runs under DIR.
 
     Expected layout (each made by the command shown in the summary):
-      DIR/prof/w<N>/   --kernel-trace --stats of the default bench run of workload N
-      DIR/pmc/w<N>_fetch, DIR/pmc/w<N>_write   FETCH_SIZE / WRITE_SIZE runs of workload N
+      DIR/prof/w<N>/, DIR/prof/p<N>/   --kernel-trace --stats of the default bench run of decode workload N,
+                                       or of `--prefill N`
+      DIR/pmc/w<N>_fetch, DIR/pmc/w<N>_write (and p<N>_...)   FETCH_SIZE / WRITE_SIZE runs of the same
       DIR/pmc/copy_fetch, DIR/pmc/copy_write   the same counters on a 256 MiB copy
     """
-    from workloads.synth import WORKLOADS, draw_new_rows, generate
+    from workloads.synth import PREFILL_WORKLOADS, WORKLOADS, generate, generate_prefill
 
     d = a.summarize
     cal_f = _counter_medians(os.path.join(d, "pmc", "copy_fetch")).get(("copy", "FETCH_SIZE"))
@@ -134,40 +137,58 @@ def summarize(a):
     fetch_scale = COPY_CAL_BYTES / 1024 / cal_f if cal_f else None
     write_scale = COPY_CAL_BYTES / 1024 / cal_w if cal_w else None
     os.makedirs(PROFILES, exist_ok=True)
-    for i, spec in WORKLOADS.items():
-        stats = _kernel_stats(os.path.join(d, "prof", f"w{i}"))
+    jobs = [("w", i, spec) for i, spec in WORKLOADS.items()] + [("p", i, spec) for i, spec in PREFILL_WORKLOADS.items()]
+    for tag, i, spec in jobs:
+        stats = _kernel_stats(os.path.join(d, "prof", f"{tag}{i}"))
         if not stats:
             continue
-        attn = [r for r in stats if "decode_" in r["Name"]]
-        w = generate(spec)
-        kv = w.kv_bytes
-        fm = _counter_medians(os.path.join(d, "pmc", f"w{i}_fetch")).get(("attn", "FETCH_SIZE"))
-        wm = _counter_medians(os.path.join(d, "pmc", f"w{i}_write")).get(("attn", "WRITE_SIZE"))
+        key = "decode_" if tag == "w" else "prefill_"
+        attn = [r for r in stats if key in r["Name"]]
+        if tag == "w":
+            w = generate(spec)
+            units = {"algorithmic_bytes": w.kv_bytes}
+            sources = KERNEL_SOURCES
+            bench_args = f"--workload {i} --cpu-seconds 0"
+            pmc_args = f"--workload {i} --timing eager --steps 4 --warmup 1 --cpu-seconds 0"
+        else:
+            pw = generate_prefill(spec)
+            units = {"algorithmic_flops": pw.flops, "kv_bytes": pw.kv.kv_bytes}
+            sources = PREFILL_SOURCES
+            bench_args = f"--prefill {i} --steps 20 --warmup 3 --cpu-seconds 0"
+            pmc_args = f"--prefill {i} --steps 3 --warmup 1 --cpu-seconds 0"
+        fm = _counter_medians(os.path.join(d, "pmc", f"{tag}{i}_fetch")).get(("attn", "FETCH_SIZE"))
+        wm = _counter_medians(os.path.join(d, "pmc", f"{tag}{i}_write")).get(("attn", "WRITE_SIZE"))
         traffic = None
         if fm and wm and fetch_scale and write_scale:
             traffic = round(fm * 1024 * fetch_scale + wm * 1024 * write_scale)
         kname = _short_kernel_name(attn[0]["Name"]) if attn else "none"
         avg_ns = float(attn[0]["AverageNs"]) if attn else None
-        rec = {"workload": spec.name, "kernel": kname, "kernel_source_hash": kernel_source_hash(),
-               "calls": int(attn[0]["Calls"]) if attn else 0, "avg_duration_us": avg_ns / 1e3 if avg_ns else None,
-               "algorithmic_bytes": kv, "achieved_GBps_from_trace": round(kv / avg_ns, 1) if avg_ns else None,
-               "fetch_KiB_per_dispatch": fm, "write_KiB_per_dispatch": wm,
-               "fetch_scale": fetch_scale, "write_scale": write_scale, "traffic_bytes": traffic,
-               "traffic_over_algorithmic": round(traffic / kv, 4) if traffic else None}
+        rec = {"workload": spec.name, "kernel": kname, "kernel_source_hash": kernel_source_hash(sources),
+               "calls": int(attn[0]["Calls"]) if attn else 0, "avg_duration_us": avg_ns / 1e3 if avg_ns else None}
+        rec.update(units)
+        if tag == "w":
+            kv = units["algorithmic_bytes"]
+            rec["achieved_GBps_from_trace"] = round(kv / avg_ns, 1) if avg_ns else None
+        else:
+            rec["achieved_TFLOPs_from_trace"] = round(units["algorithmic_flops"] / avg_ns / 1e3, 1) if avg_ns else None
+            kv = units["kv_bytes"]
+        rec.update({"fetch_KiB_per_dispatch": fm, "write_KiB_per_dispatch": wm, "fetch_scale": fetch_scale,
+                    "write_scale": write_scale, "traffic_bytes": traffic,
+                    "traffic_over_kv_bytes": round(traffic / kv, 4) if traffic else None})
         name = f"{kname}_{spec.name}.md"
         with open(os.path.join(PROFILES, name), "w") as f:
             f.write(f"# {kname} on {spec.name}\n\n")
             f.write("Commands (run from the repository root on the MI355X box, after `cd /tmp && export TMPDIR=/tmp`"
                     " and returning to the root):\n\n```\n")
-            f.write(f"rocprofv3 --kernel-trace --stats --output-format csv -d {d}/prof/w{i} -o w{i} -- "
-                    f"python bench.py --workload {i} --cpu-seconds 0\n")
+            f.write(f"rocprofv3 --kernel-trace --stats --output-format csv -d {d}/prof/{tag}{i} -o {tag}{i} -- "
+                    f"python3 bench.py {bench_args}\n")
             for c in ("FETCH_SIZE", "WRITE_SIZE"):
                 sub = "fetch" if c == "FETCH_SIZE" else "write"
-                f.write(f"rocprofv3 --pmc {c} --output-format csv -d {d}/pmc/w{i}_{sub} -o w{i}_{sub} -- "
-                        f"python bench.py --workload {i} --timing eager --steps 4 --warmup 1 --cpu-seconds 0\n")
+                f.write(f"rocprofv3 --pmc {c} --output-format csv -d {d}/pmc/{tag}{i}_{sub} -o {tag}{i}_{sub} -- "
+                        f"python3 bench.py {pmc_args}\n")
                 f.write(f"rocprofv3 --pmc {c} --output-format csv -d {d}/pmc/copy_{sub} -o copy_{sub} -- "
-                        f"python bench.py --probe copy --probe-bytes {COPY_CAL_BYTES} --steps 3 --warmup 1\n")
-            f.write(f"python bench.py --summarize {d}\n```\n\n")
+                        f"python3 bench.py --probe copy --probe-bytes {COPY_CAL_BYTES} --steps 3 --warmup 1\n")
+            f.write(f"python3 bench.py --summarize {d}\n```\n\n")
             f.write("Kernel statistics (rocprofv3 --stats, all dispatches of the bench run):\n\n")
             f.write("| kernel | calls | avg us | min us | max us |\n|---|---|---|---|---|\n")
             for r in stats:
@@ -179,14 +200,15 @@ def summarize(a):
         print(f"wrote profiles/{name}", flush=True)
 
 
-def recorded_traffic(workload_name):
+def recorded_traffic(workload_name, sources=KERNEL_SOURCES, unit_key="algorithmic_bytes"):
     """HBM bytes per dispatch from a profiles/ summary of the current kernel sources, else None."""
     for f in glob.glob(os.path.join(PROFILES, f"*_{workload_name}.md")):
         txt = open(f).read()
         if "```json" not in txt:
             continue
         rec = json.loads(txt.split("```json", 1)[1].split("```", 1)[0])
-        if rec.get("kernel_source_hash") == kernel_source_hash() and rec.get("traffic_bytes"):
+        if rec.get("kernel_source_hash") == kernel_source_hash(sources) and rec.get("traffic_bytes") and \
+                unit_key in rec:
             return rec["traffic_bytes"]
     return None
 
@@ -352,7 +374,8 @@ def _prefill(a):
                    "page_size": s.page_size, "new_tokens": int(pw.q_lens.sum()),
                    "cached_tokens": int(pw.kv.ctx_lens.sum()), "flops_per_step": flops, "timing": "eager"},
         "roofline": {"bound": "mfma", "achieved": round(tflops, 3), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-                     "frac": round(tflops / PEAK_BF16_TFLOPS, 4), "traffic": None},
+                     "frac": round(tflops / PEAK_BF16_TFLOPS, 4),
+                     "traffic": recorded_traffic(pspec.name, PREFILL_SOURCES, "algorithmic_flops")},
         "cpu_baseline": cpu,
     }), flush=True)
 
