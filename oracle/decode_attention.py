@@ -27,6 +27,11 @@ token ranges and merging the partial results with their log-sum-exps; the
 merge is also written out here (``lse_combine``) so it can be checked against
 unsplit attention. Every value is float64, computed on the exact values the
 GPU sees (bf16 bit patterns are widened exactly).
+
+FP8 KV caches (KV quantization, the prior art the paper cites next to KV
+eviction) store OCP FP8 E4M3 codes with a per-tensor scale; the attended
+keys and values are the decoded codes times that scale (``dequantize``),
+and the attention itself is unchanged.
 """
 
 from __future__ import annotations
@@ -37,14 +42,37 @@ from typing import Iterable, List, Optional, Sequence, Tuple
 import numpy as np
 
 
+def fp8_e4m3_value(codes: np.ndarray) -> np.ndarray:
+    """Float64 values of OCP FP8 E4M3 codes (uint8), from the format's definition.
+
+    Sign bit 7, exponent bits 6..3 (bias 7), mantissa bits 2..0. Exponent 0
+    is subnormal: m/8 * 2^-6. Otherwise (1 + m/8) * 2^(e - 7). Exponent 15
+    with mantissa 7 is NaN; the format has no infinities (max 448).
+    """
+    c = np.asarray(codes, dtype=np.uint8).astype(np.int64)
+    sign = np.where(c >> 7, -1.0, 1.0)
+    e = (c >> 3) & 15
+    m = (c & 7).astype(np.float64)
+    mag = np.where(e == 0, m / 8.0 * 2.0 ** -6, (1.0 + m / 8.0) * np.exp2(e - 7.0))
+    return np.where((e == 15) & (m == 7), np.nan, sign * mag)
+
+
 def widen(x: np.ndarray, dtype: str) -> np.ndarray:
-    """Exact float64 values of the stored data (``dtype`` "bf16": uint16 bit patterns)."""
+    """Exact float64 values of the stored data ("bf16": uint16 bit patterns; "fp8": E4M3 codes, unscaled)."""
     if dtype == "f32":
         return np.asarray(x, dtype=np.float32).astype(np.float64)
     if dtype == "bf16":
         bits = np.asarray(x, dtype=np.uint16).astype(np.uint32) << np.uint32(16)
         return bits.view(np.float32).astype(np.float64)
+    if dtype == "fp8":
+        return fp8_e4m3_value(x)
     raise ValueError(f"unknown dtype {dtype!r}")
+
+
+def dequantize(x: np.ndarray, dtype: str, scale: float = 1.0) -> np.ndarray:
+    """Float64 K or V values as attended: the stored values, times the tensor's scale for fp8."""
+    v = widen(x, dtype)
+    return v * float(scale) if dtype == "fp8" else v
 
 
 def attend(q_rows: np.ndarray, keys: np.ndarray, values: np.ndarray,
@@ -167,12 +195,15 @@ def append_paged(kv_pages: np.ndarray, block_table: np.ndarray, ctx_lens: np.nda
 
 
 def _attend_sequence(q_b: np.ndarray, keys: np.ndarray, values: np.ndarray, dtype: str,
-                     scale: float, heads: Optional[Iterable[int]] = None):
-    """All (or selected) query heads of one sequence; keys/values are [L, Hkv, D] stored values."""
+                     scale: float, heads: Optional[Iterable[int]] = None, kv_scales=(1.0, 1.0)):
+    """All (or selected) query heads of one sequence; keys/values are [L, Hkv, D] stored values.
+
+    dtype "fp8": q is bf16, K and V are E4M3 codes scaled by kv_scales = (k_scale, v_scale).
+    """
     Hq, D = q_b.shape
     Hkv = keys.shape[1]
     G = Hq // Hkv
-    qf = widen(q_b, dtype)
+    qf = widen(q_b, "bf16" if dtype == "fp8" else dtype)
     want = set(range(Hq)) if heads is None else set(heads)
     out = np.zeros((Hq, D))
     lse = np.full(Hq, -np.inf)
@@ -180,8 +211,8 @@ def _attend_sequence(q_b: np.ndarray, keys: np.ndarray, values: np.ndarray, dtyp
         hs = [h for h in range(hk * G, (hk + 1) * G) if h in want]
         if not hs:
             continue
-        kf = widen(keys[:, hk], dtype)
-        vf = widen(values[:, hk], dtype)
+        kf = dequantize(keys[:, hk], dtype, kv_scales[0])
+        vf = dequantize(values[:, hk], dtype, kv_scales[1])
         o, l = attend(qf[hs], kf, vf, scale)
         out[hs] = o
         lse[hs] = l
@@ -189,7 +220,7 @@ def _attend_sequence(q_b: np.ndarray, keys: np.ndarray, values: np.ndarray, dtyp
 
 
 def decode_attention(q: np.ndarray, k: np.ndarray, v: np.ndarray, seq_start: np.ndarray,
-                     ctx_lens: np.ndarray, scale: float, dtype: str):
+                     ctx_lens: np.ndarray, scale: float, dtype: str, kv_scales=(1.0, 1.0)):
     """Contiguous/ragged layout: q [B, Hq, D]; k, v [T, Hkv, D]. Returns out [B,Hq,D], lse [B,Hq]."""
     B, Hq, D = q.shape
     if Hq % k.shape[1] != 0:
@@ -198,12 +229,14 @@ def decode_attention(q: np.ndarray, k: np.ndarray, v: np.ndarray, seq_start: np.
     lse = np.full((B, Hq), -np.inf)
     for b in range(B):
         out[b], lse[b] = _attend_sequence(q[b], contiguous_context(k, seq_start, ctx_lens, b),
-                                          contiguous_context(v, seq_start, ctx_lens, b), dtype, scale)
+                                          contiguous_context(v, seq_start, ctx_lens, b), dtype, scale,
+                                          kv_scales=kv_scales)
     return out, lse
 
 
 def decode_attention_paged(q: np.ndarray, k_pages: np.ndarray, v_pages: np.ndarray,
-                           block_table: np.ndarray, ctx_lens: np.ndarray, scale: float, dtype: str):
+                           block_table: np.ndarray, ctx_lens: np.ndarray, scale: float, dtype: str,
+                           kv_scales=(1.0, 1.0)):
     """Paged layout: k_pages, v_pages [P, page_size, Hkv, D]; block_table [B, max_pages]."""
     B, Hq, D = q.shape
     if Hq % k_pages.shape[2] != 0:
@@ -212,7 +245,8 @@ def decode_attention_paged(q: np.ndarray, k_pages: np.ndarray, v_pages: np.ndarr
     lse = np.full((B, Hq), -np.inf)
     for b in range(B):
         out[b], lse[b] = _attend_sequence(q[b], paged_context(k_pages, block_table, ctx_lens, b),
-                                          paged_context(v_pages, block_table, ctx_lens, b), dtype, scale)
+                                          paged_context(v_pages, block_table, ctx_lens, b), dtype, scale,
+                                          kv_scales=kv_scales)
     return out, lse
 
 
@@ -231,7 +265,8 @@ def decode_attention_rows(workload, rows: Sequence[Tuple[int, int]]) -> List[Tup
         else:
             keys = contiguous_context(workload.k, workload.seq_start, workload.ctx_lens, b)
             values = contiguous_context(workload.v, workload.seq_start, workload.ctx_lens, b)
-        o, l = _attend_sequence(workload.q[b], keys, values, spec.dtype, float(spec.scale), heads=hs)
+        o, l = _attend_sequence(workload.q[b], keys, values, spec.dtype, float(spec.scale), heads=hs,
+                                kv_scales=kv_scales_of(spec))
         for h in hs:
             cache[(b, h)] = (o[h], float(l[h]))
     for b, h in rows:
@@ -239,11 +274,17 @@ def decode_attention_rows(workload, rows: Sequence[Tuple[int, int]]) -> List[Tup
     return results
 
 
+def kv_scales_of(spec):
+    """(k_scale, v_scale) of a workload spec: its FP8 scales, else (1, 1)."""
+    return (float(spec.k_scale), float(spec.v_scale)) if spec.dtype == "fp8" else (1.0, 1.0)
+
+
 def reference(workload):
     """Full oracle result (out [B,Hq,D] float64, lse [B,Hq] float64) for a drawn workload."""
     spec = workload.spec
     if spec.layout == "paged":
         return decode_attention_paged(workload.q, workload.k_pages, workload.v_pages,
-                                      workload.block_table, workload.ctx_lens, float(spec.scale), spec.dtype)
+                                      workload.block_table, workload.ctx_lens, float(spec.scale), spec.dtype,
+                                      kv_scales=kv_scales_of(spec))
     return decode_attention(workload.q, workload.k, workload.v, workload.seq_start, workload.ctx_lens,
-                            float(spec.scale), spec.dtype)
+                            float(spec.scale), spec.dtype, kv_scales=kv_scales_of(spec))

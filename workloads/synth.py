@@ -26,7 +26,12 @@ Recipe (every choice that the paper leaves open):
     unused block-table entries are -1;
   * "5% of keys scaled x8" is a Bernoulli(0.05) draw per (pool token slot,
     KV head) row of K only; the whole head_dim vector is scaled before the
-    bf16 cast (x8 is a power of two, so before/after the cast agree).
+    bf16 cast (x8 is a power of two, so before/after the cast agree);
+  * FP8 KV workloads (dtype "fp8"): q is drawn as for bf16; K and V are the
+    same N(0, 1) draws divided by a per-tensor scale (k_scale, v_scale, a
+    power of two by default, so the division is exact) and rounded to the
+    nearest OCP FP8 E4M3 code (ties to even, by torch's float8_e4m3fn cast);
+    the cache stores the codes and the scales travel with the workload.
 """
 
 from __future__ import annotations
@@ -56,7 +61,7 @@ class WorkloadSpec:
     num_q_heads: int
     num_kv_heads: int
     head_dim: int
-    dtype: str  # "f32" or "bf16": dtype of q, K and V alike
+    dtype: str  # "f32" or "bf16" (q, K and V alike) or "fp8" (q bf16, K and V OCP FP8 E4M3 codes)
     lengths: tuple  # ("fixed", L) or ("uniform", lo, hi) or ("list", (L0, L1, ...))
     max_ctx_len: int  # upper bound on every length (planning / block-table width)
     layout: str = "contiguous"  # "contiguous" (packed ragged) or "paged"
@@ -64,6 +69,8 @@ class WorkloadSpec:
     key_scale_frac: float = 0.0
     key_scale: float = 8.0
     seed: int = 0
+    k_scale: float = 2.0 ** -6  # fp8 only: K = code value * k_scale
+    v_scale: float = 2.0 ** -6  # fp8 only: V = code value * v_scale
 
     @property
     def group(self) -> int:
@@ -76,7 +83,12 @@ class WorkloadSpec:
 
     @property
     def elem_bytes(self) -> int:
-        return 4 if self.dtype == "f32" else 2
+        """Bytes of one K or V element."""
+        return {"f32": 4, "bf16": 2, "fp8": 1}[self.dtype]
+
+    @property
+    def q_dtype(self) -> str:
+        return "bf16" if self.dtype == "fp8" else self.dtype
 
     def replace(self, **kw) -> "WorkloadSpec":
         return dataclasses.replace(self, **kw)
@@ -93,7 +105,24 @@ WORKLOADS = {
                     key_scale_frac=0.05, seed=1004),
     5: WorkloadSpec("bf16_paged64_B8_L131072_G8", 8, 64, 8, 128, "bf16",
                     ("fixed", 131072), 131072, layout="paged", page_size=64, seed=1005),
+    # FP8 KV variants of the headline and the longest shapes (KV quantization, an extension row)
+    6: WorkloadSpec("fp8_B1_L32768", 1, 32, 8, 128, "fp8", ("fixed", 32768), 32768, seed=1006),
+    7: WorkloadSpec("fp8_paged64_B8_L131072_G8", 8, 64, 8, 128, "fp8",
+                    ("fixed", 131072), 131072, layout="paged", page_size=64, seed=1007),
 }
+
+
+def f32_to_fp8_e4m3_codes(x: np.ndarray) -> np.ndarray:
+    """Round float32 values to the nearest OCP FP8 E4M3 code (ties to even) with torch's cast.
+
+    Values must lie within the format's range (|x| <= 448); the codes are returned as uint8.
+    """
+    import torch
+
+    x = np.ascontiguousarray(x, dtype=np.float32)
+    if np.abs(x).max(initial=0.0) > 448.0:
+        raise ValueError("value outside the FP8 E4M3 range")
+    return torch.from_numpy(x).to(torch.float8_e4m3fn).view(torch.uint8).numpy()
 
 
 def f32_to_bf16_bits(x: np.ndarray) -> np.ndarray:
@@ -110,18 +139,19 @@ def f32_to_bf16_bits(x: np.ndarray) -> np.ndarray:
 
 
 def _draw_tensor(stream: np.random.SeedSequence, shape, dtype: str,
-                 row_scale: Optional[np.ndarray] = None) -> np.ndarray:
+                 row_scale: Optional[np.ndarray] = None, quant_scale: float = 1.0) -> np.ndarray:
     """N(0,1) tensor drawn in fixed chunks of _DRAW_CHUNK elements.
 
     Chunk c is drawn from its own generator seeded by ``stream.spawn(n)[c]``, so
     the values depend only on the seed and the shape, never on the thread count.
     ``row_scale`` (optional) multiplies each row (all leading dims but the last)
-    before the bf16 cast.
+    before the bf16 cast. For "fp8" the draws are divided by ``quant_scale``
+    and rounded to FP8 E4M3 codes.
     """
     n = int(np.prod(shape))
     inner = shape[-1]
     assert _DRAW_CHUNK % inner == 0
-    out = np.empty(n, dtype=np.float32 if dtype == "f32" else np.uint16)
+    out = np.empty(n, dtype={"f32": np.float32, "bf16": np.uint16, "fp8": np.uint8}[dtype])
     nchunks = max(1, -(-n // _DRAW_CHUNK))
     children = stream.spawn(nchunks)
     rs = None if row_scale is None else row_scale.reshape(-1)
@@ -132,7 +162,12 @@ def _draw_tensor(stream: np.random.SeedSequence, shape, dtype: str,
         x = np.random.default_rng(children[c]).standard_normal(hi - lo, dtype=np.float32)
         if rs is not None:
             x = (x.reshape(-1, inner) * rs[lo // inner: hi // inner, None]).reshape(-1)
-        out[lo:hi] = x if dtype == "f32" else f32_to_bf16_bits(x)
+        if dtype == "f32":
+            out[lo:hi] = x
+        elif dtype == "bf16":
+            out[lo:hi] = f32_to_bf16_bits(x)
+        else:
+            out[lo:hi] = f32_to_fp8_e4m3_codes(x / np.float32(quant_scale))
 
     if nchunks == 1:
         work(0)
@@ -196,8 +231,11 @@ def generate(spec: WorkloadSpec, seed: Optional[int] = None, *, gap_rows: int = 
     B, Hq, Hkv, D = spec.batch, spec.num_q_heads, spec.num_kv_heads, spec.head_dim
     assert Hq % Hkv == 0
     lens = draw_lengths(spec, rng["lengths"])
-    q = _draw_tensor(seqs["q"], (B, Hq, D), spec.dtype)
-    nan_bits = np.float32("nan") if spec.dtype == "f32" else np.uint16(0x7FC0)
+    q = _draw_tensor(seqs["q"], (B, Hq, D), spec.q_dtype)
+    nan_bits = {"f32": np.float32("nan"), "bf16": np.uint16(0x7FC0), "fp8": np.uint8(0x7F)}[spec.dtype]
+    if spec.dtype == "fp8" and spec.key_scale_frac > 0:
+        raise ValueError("scaled keys are not drawn for fp8 workloads")
+    kq, vq = (spec.k_scale, spec.v_scale) if spec.dtype == "fp8" else (1.0, 1.0)
 
     if spec.layout == "contiguous":
         starts = np.zeros(B, dtype=np.int64)
@@ -211,8 +249,8 @@ def generate(spec: WorkloadSpec, seed: Optional[int] = None, *, gap_rows: int = 
         if spec.key_scale_frac > 0:
             mask = np.where(rng["key_mask"].random(rows) < spec.key_scale_frac,
                             np.float32(spec.key_scale), np.float32(1.0))
-        k = _draw_tensor(seqs["k"], (T, Hkv, D), spec.dtype, mask)
-        v = _draw_tensor(seqs["v"], (T, Hkv, D), spec.dtype)
+        k = _draw_tensor(seqs["k"], (T, Hkv, D), spec.dtype, mask, quant_scale=kq)
+        v = _draw_tensor(seqs["v"], (T, Hkv, D), spec.dtype, quant_scale=vq)
         if poison:
             covered = np.zeros(T, dtype=bool)
             for b in range(B):
@@ -242,8 +280,8 @@ def generate(spec: WorkloadSpec, seed: Optional[int] = None, *, gap_rows: int = 
     if spec.key_scale_frac > 0:
         mask = np.where(rng["key_mask"].random(rows) < spec.key_scale_frac,
                         np.float32(spec.key_scale), np.float32(1.0))
-    kp = _draw_tensor(seqs["k"], (P, ps, Hkv, D), spec.dtype, mask)
-    vp = _draw_tensor(seqs["v"], (P, ps, Hkv, D), spec.dtype)
+    kp = _draw_tensor(seqs["k"], (P, ps, Hkv, D), spec.dtype, mask, quant_scale=kq)
+    vp = _draw_tensor(seqs["v"], (P, ps, Hkv, D), spec.dtype, quant_scale=vq)
     if poison:
         covered = np.zeros((P, ps), dtype=bool)
         for b in range(B):
@@ -255,10 +293,12 @@ def generate(spec: WorkloadSpec, seed: Optional[int] = None, *, gap_rows: int = 
 
 
 def draw_new_rows(spec: WorkloadSpec, seed: int):
-    """The new token's key and value rows for every sequence: two [B, Hkv, D] tensors ~ N(0,1) in spec.dtype."""
+    """The new token's key and value rows for every sequence: two [B, Hkv, D] tensors ~ N(0,1) in spec.dtype
+    (fp8: divided by k_scale / v_scale and rounded to codes)."""
     ks, vs = np.random.SeedSequence(seed).spawn(2)
     shape = (spec.batch, spec.num_kv_heads, spec.head_dim)
-    return _draw_tensor(ks, shape, spec.dtype), _draw_tensor(vs, shape, spec.dtype)
+    kq, vq = (spec.k_scale, spec.v_scale) if spec.dtype == "fp8" else (1.0, 1.0)
+    return (_draw_tensor(ks, shape, spec.dtype, quant_scale=kq), _draw_tensor(vs, shape, spec.dtype, quant_scale=vq))
 
 
 # ---------------------------------------------------------------- prefill workloads
