@@ -47,7 +47,8 @@ def _args():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=20)
-    ap.add_argument("--workload", type=int, default=2, help="named workload 1..5 (2 = the headline one)")
+    ap.add_argument("--workload", type=int, default=2,
+                    help="named workload 1..7 (2 = the headline one; 6, 7 = FP8 KV variants of 2 and 5)")
     ap.add_argument("--op", default="attention", choices=["attention", "append", "step", "fused"],
                     help="attention: the decode-attention call; append: the KV-append call alone; "
                          "step: the append call then the attention call; fused: both in one launch")
@@ -407,12 +408,12 @@ def main():
     kv_bytes = w.kv_bytes
     dev = torch.device("cuda:0")
 
-    def dev_t(x):
-        if spec.dtype == "bf16":
+    def dev_t(x, dtype=spec.dtype):
+        if dtype == "bf16":
             return torch.from_numpy(np.ascontiguousarray(x).view(np.int16)).view(torch.bfloat16).to(dev)
-        return torch.from_numpy(np.ascontiguousarray(x)).to(dev)
+        return torch.from_numpy(np.ascontiguousarray(x)).to(dev)  # f32 values or fp8 codes (uint8)
 
-    q = dev_t(w.q)
+    q = dev_t(w.q, spec.q_dtype)
     ctx = torch.from_numpy(w.ctx_lens.astype(np.int32)).to(dev)
     copies = a.copies or max(1, math.ceil(4 * MALL_BYTES / kv_bytes))
     paged = spec.layout == "paged"
@@ -423,8 +424,9 @@ def main():
         bt = torch.from_numpy(w.block_table.astype(np.int32)).to(dev)
     else:
         ss = torch.from_numpy(w.seq_start.astype(np.int64)).to(dev)
+    scales = dict(k_scale=spec.k_scale, v_scale=spec.v_scale) if spec.dtype == "fp8" else {}
     op = DecodeAttention(spec.num_q_heads, spec.num_kv_heads, spec.head_dim, spec.dtype, float(spec.scale),
-                         spec.batch, spec.max_ctx_len, chunk_tokens=a.chunk, variant=a.variant)
+                         spec.batch, spec.max_ctx_len, chunk_tokens=a.chunk, variant=a.variant, **scales)
     chunk, splits = op.splits(spec.batch, spec.max_ctx_len)
     out = torch.zeros((spec.batch, spec.num_q_heads, spec.head_dim), dtype=torch.float32, device=dev)
     lse = torch.empty((spec.batch, spec.num_q_heads), dtype=torch.float32, device=dev)
@@ -511,7 +513,7 @@ def main():
     assert torch.isfinite(out).all().item()
 
     cpu = _cpu_baseline(w, a.cpu_seconds) if a.cpu_seconds > 0 and a.op == "attention" else None
-    kind = a.variant if a.variant != "auto" else ("mfma" if spec.dtype == "bf16" else "valu")
+    kind = a.variant if a.variant != "auto" else ("valu" if spec.dtype == "f32" else "mfma")
     line = {
         "metric": METRIC,
         "value": round(gbps, 2),

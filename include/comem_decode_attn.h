@@ -62,14 +62,17 @@ typedef enum {
 } comem_status;
 
 typedef enum {
-  COMEM_F32 = 0, /* q, K, V in IEEE float32 */
-  COMEM_BF16 = 1 /* q, K, V in bfloat16 */
+  COMEM_F32 = 0,     /* q, K, V in IEEE float32 */
+  COMEM_BF16 = 1,    /* q, K, V in bfloat16 */
+  COMEM_FP8_E4M3 = 2 /* q in bfloat16; K and V as OCP FP8 E4M3 codes (one byte, bias 7, no
+                        infinities), attended as code value * k_scale and code value * v_scale
+                        (KV quantization, the prior art the paper cites beside KV eviction) */
 } comem_dtype;
 
 typedef enum {
-  COMEM_VARIANT_AUTO = 0,     /* bf16 -> matrix-core kernel; f32 -> vector kernel */
+  COMEM_VARIANT_AUTO = 0,     /* bf16, fp8 -> matrix-core kernel; f32 -> vector kernel */
   COMEM_VARIANT_VALU = 1,     /* vector-ALU kernel (f32 and bf16), one workgroup per split */
-  COMEM_VARIANT_MFMA = 2,     /* matrix-core kernel (bf16 only); persistent workgroups take
+  COMEM_VARIANT_MFMA = 2,     /* matrix-core kernel (bf16, fp8); persistent workgroups take
                                  splits from a work queue when a workspace is given and
                                  batch <= 4096, else one workgroup per split */
   COMEM_VARIANT_MFMA_GRID = 3 /* matrix-core kernel, always one workgroup per split */
@@ -85,12 +88,14 @@ typedef struct {
   int32_t num_q_heads;  /* h_q > 0 */
   int32_t num_kv_heads; /* h_kv > 0, h_q % h_kv == 0, G = h_q / h_kv in {1,2,4,8,16} */
   int32_t head_dim;     /* d_h in {64, 128} */
-  int32_t dtype;        /* comem_dtype of q, K and V */
+  int32_t dtype;        /* comem_dtype of q, K and V (see COMEM_FP8_E4M3 for the FP8 cache) */
   float scale;          /* softmax scale, finite and > 0 (1/sqrt(d_h) is usual) */
   int32_t max_batch;    /* largest batch any call will pass (> 0) */
   int64_t max_ctx_len;  /* largest context any call will pass (> 0) */
   int32_t chunk_tokens; /* tokens per split: 0 = planned per call; else a multiple of 32 */
-  int32_t variant;      /* comem_variant */
+  int32_t variant;      /* comem_variant (fp8 caches: not COMEM_VARIANT_VALU) */
+  float k_scale;        /* COMEM_FP8_E4M3 only: finite and > 0, the per-tensor K scale */
+  float v_scale;        /* COMEM_FP8_E4M3 only: finite and > 0, the per-tensor V scale */
 } comem_decode_attn_config;
 
 typedef struct comem_decode_attn_plan comem_decode_attn_plan;
@@ -119,8 +124,10 @@ comem_status comem_decode_attn_plan_splits(const comem_decode_attn_plan* plan, i
                                            int32_t* chunk_tokens_out, int32_t* num_splits_out);
 
 /* Contiguous / ragged cache (paper Sec. 2.2: K_cache, V_cache of l tokens,
- * each token an [h_kv, d_h] block).
- *   q          [batch, h_q, d_h] dense, dtype of the plan, 16-byte aligned.
+ * each token an [h_kv, d_h] block). Strides count elements of the cache's
+ * dtype (bytes for FP8 caches).
+ *   q          [batch, h_q, d_h] dense, dtype of the plan (bf16 for FP8
+ *              caches), 16-byte aligned.
  *   k, v       element (b, t, hk, d) at k[(seq_start[b] + t) * stride_token
  *              + hk * stride_head + d]; d contiguous. 16-byte aligned; the
  *              byte sizes of both strides must be multiples of 16.
@@ -165,7 +172,7 @@ comem_status comem_decode_attn_paged(const comem_decode_attn_plan* plan, const v
  * cache element is left as it was. Run on the same stream before the
  * attention call, it gives the append-then-attend order of a decode step.
  * The rows are copied, so the stored bits equal the given ones.
- *   new_k, new_v device [batch, h_kv, d_h] dense, dtype of the plan, 16-byte aligned.
+ *   new_k, new_v device [batch, h_kv, d_h] dense, the cache's dtype (FP8 caches: codes), 16-byte aligned.
  *   k, v          the cache (written), addressed as in comem_decode_attn.
  *   max_ctx_len   host bound, <= plan max_ctx_len.
  * A sequence whose ctx_lens[b] is outside [1, max_ctx_len] (or, paged,

@@ -21,7 +21,8 @@ PROBE_LIB_PATH = os.path.join(PKG, "libcomem_probe.so")
 
 OK, ERR_NULL_POINTER, ERR_INVALID_SHAPE, ERR_UNSUPPORTED, ERR_MISALIGNED = 0, 1, 2, 3, 4
 ERR_WORKSPACE_TOO_SMALL, ERR_BAD_HANDLE, ERR_HIP, ERR_NO_DEVICE = 5, 6, 7, 8
-F32, BF16 = 0, 1
+F32, BF16, FP8_E4M3 = 0, 1, 2
+DTYPES = {"f32": F32, "bf16": BF16, "fp8": FP8_E4M3}
 VARIANT_AUTO, VARIANT_VALU, VARIANT_MFMA, VARIANT_MFMA_GRID = 0, 1, 2, 3
 NO_DEVICE = -1
 
@@ -49,6 +50,8 @@ class Config(ctypes.Structure):
         ("max_ctx_len", ctypes.c_int64),
         ("chunk_tokens", ctypes.c_int32),
         ("variant", ctypes.c_int32),
+        ("k_scale", ctypes.c_float),
+        ("v_scale", ctypes.c_float),
     ]
 
 
@@ -291,18 +294,19 @@ class DecodeAttention:
 
     q: [B, Hq, D]; contiguous k, v: [T, Hkv, D] (any strides with d
     contiguous); paged k, v: [P, page_size, Hkv, D]. Outputs are float32
-    [B, Hq, D] and [B, Hq] (natural-log lse).
+    [B, Hq, D] and [B, Hq] (natural-log lse). dtype "fp8": q is bf16, K and V
+    are uint8 tensors of OCP FP8 E4M3 codes with per-tensor k_scale, v_scale.
     """
 
     def __init__(self, num_q_heads: int, num_kv_heads: int, head_dim: int, dtype: str, scale: float,
                  max_batch: int, max_ctx_len: int, chunk_tokens: int = 0, variant: str = "auto",
-                 device: int = 0):
+                 device: int = 0, k_scale: float = 1.0, v_scale: float = 1.0):
         import torch
 
-        self.cfg = Config(num_q_heads, num_kv_heads, head_dim, BF16 if dtype == "bf16" else F32, float(scale),
+        self.cfg = Config(num_q_heads, num_kv_heads, head_dim, DTYPES[dtype], float(scale),
                           max_batch, max_ctx_len, chunk_tokens,
                           {"auto": VARIANT_AUTO, "valu": VARIANT_VALU, "mfma": VARIANT_MFMA,
-                           "mfma_grid": VARIANT_MFMA_GRID}[variant])
+                           "mfma_grid": VARIANT_MFMA_GRID}[variant], float(k_scale), float(v_scale))
         self.device = device
         self.plan, self.workspace_bytes = comem_decode_attn_init(self.cfg, device)
         self.workspace = torch.zeros(max(self.workspace_bytes, 256), dtype=torch.uint8, device=f"cuda:{device}")

@@ -16,8 +16,8 @@
 namespace comem {
 using KernelFn = void (*)(AttnParams);
 using QueueKernelFn = void (*)(AttnParams, int);
-KernelFn select_mfma_kernel(int head_dim, bool paged, int page_size);
-QueueKernelFn select_mfma_queue_kernel(int head_dim, bool paged, int page_size);
+KernelFn select_mfma_kernel(int head_dim, bool paged, int page_size, bool fp8);
+QueueKernelFn select_mfma_queue_kernel(int head_dim, bool paged, int page_size, bool fp8);
 int mfma_max_split_pages();
 int mfma_max_queue_batch();
 KernelFn select_valu_kernel(bool bf16, int head_dim, int group, bool paged);
@@ -54,7 +54,11 @@ namespace {
 
 int group_of(const comem_decode_attn_config& c) { return c.num_q_heads / c.num_kv_heads; }
 bool uses_mfma(const comem_decode_attn_plan& p);
-int elem_bytes(const comem_decode_attn_config& c) { return c.dtype == COMEM_F32 ? 4 : 2; }
+// Bytes of one K or V element (q is bf16 for FP8 caches).
+int elem_bytes(const comem_decode_attn_config& c) {
+  return c.dtype == COMEM_F32 ? 4 : (c.dtype == COMEM_FP8_E4M3 ? 1 : 2);
+}
+bool is_fp8(const comem_decode_attn_config& c) { return c.dtype == COMEM_FP8_E4M3; }
 
 // Workspace bytes for `slots` (sequence, split) partial results: ticket
 // counters, then per-head lse values, then per-head partial outputs.
@@ -115,7 +119,7 @@ comem_status validate_config(const comem_decode_attn_config& c) {
   const int G = group_of(c);
   if (G != 1 && G != 2 && G != 4 && G != 8 && G != 16) return COMEM_ERR_UNSUPPORTED;
   if (c.head_dim != 64 && c.head_dim != 128) return COMEM_ERR_UNSUPPORTED;
-  if (c.dtype != COMEM_F32 && c.dtype != COMEM_BF16) return COMEM_ERR_UNSUPPORTED;
+  if (c.dtype != COMEM_F32 && c.dtype != COMEM_BF16 && c.dtype != COMEM_FP8_E4M3) return COMEM_ERR_UNSUPPORTED;
   if (!std::isfinite(c.scale) || !(c.scale > 0.f)) return COMEM_ERR_INVALID_SHAPE;
   if (c.max_batch <= 0 || c.max_batch > kGridYZLimit) return COMEM_ERR_INVALID_SHAPE;
   if (c.max_ctx_len <= 0 || c.max_ctx_len > kMaxContext) return COMEM_ERR_INVALID_SHAPE;
@@ -124,8 +128,13 @@ comem_status validate_config(const comem_decode_attn_config& c) {
   if (c.variant != COMEM_VARIANT_AUTO && c.variant != COMEM_VARIANT_VALU && c.variant != COMEM_VARIANT_MFMA &&
       c.variant != COMEM_VARIANT_MFMA_GRID)
     return COMEM_ERR_UNSUPPORTED;
-  if ((c.variant == COMEM_VARIANT_MFMA || c.variant == COMEM_VARIANT_MFMA_GRID) && c.dtype != COMEM_BF16)
+  if ((c.variant == COMEM_VARIANT_MFMA || c.variant == COMEM_VARIANT_MFMA_GRID) && c.dtype == COMEM_F32)
     return COMEM_ERR_UNSUPPORTED;
+  if (c.dtype == COMEM_FP8_E4M3) {
+    if (c.variant == COMEM_VARIANT_VALU) return COMEM_ERR_UNSUPPORTED;
+    if (!std::isfinite(c.k_scale) || !(c.k_scale > 0.f) || !std::isfinite(c.v_scale) || !(c.v_scale > 0.f))
+      return COMEM_ERR_INVALID_SHAPE;
+  }
   return COMEM_OK;
 }
 
@@ -176,7 +185,7 @@ comem_status validate_common(const comem_decode_attn_plan& p, const void* q, con
 
 bool uses_mfma(const comem_decode_attn_plan& p) {
   return p.cfg.variant == COMEM_VARIANT_MFMA || p.cfg.variant == COMEM_VARIANT_MFMA_GRID ||
-         (p.cfg.variant == COMEM_VARIANT_AUTO && p.cfg.dtype == COMEM_BF16);
+         (p.cfg.variant == COMEM_VARIANT_AUTO && p.cfg.dtype != COMEM_F32);
 }
 
 // The work-queue form of the matrix-core kernel keeps two counters after the
@@ -194,7 +203,7 @@ comem_status launch(const comem_decode_attn_plan& p, bool paged, comem::AttnPara
   // With no more (nominal) items than resident workgroups every item gets its
   // own workgroup anyway, and the grid form saves the queue's prologue.
   if (queue && items > resident) {
-    comem::QueueKernelFn qfn = comem::select_mfma_queue_kernel(p.cfg.head_dim, paged, a.page_mask + 1);
+    comem::QueueKernelFn qfn = comem::select_mfma_queue_kernel(p.cfg.head_dim, paged, a.page_mask + 1, is_fp8(p.cfg));
     if (qfn == nullptr) return COMEM_ERR_UNSUPPORTED;
     dim3 grid(static_cast<unsigned>(items < resident ? items : resident));
     dim3 block(comem::kThreads);
@@ -204,7 +213,7 @@ comem_status launch(const comem_decode_attn_plan& p, bool paged, comem::AttnPara
                                            static_cast<hipStream_t>(stream));
     return err == hipSuccess ? COMEM_OK : COMEM_ERR_HIP;
   }
-  comem::KernelFn fn = uses_mfma(p) ? comem::select_mfma_kernel(p.cfg.head_dim, paged, a.page_mask + 1)
+  comem::KernelFn fn = uses_mfma(p) ? comem::select_mfma_kernel(p.cfg.head_dim, paged, a.page_mask + 1, is_fp8(p.cfg))
                                     : comem::select_valu_kernel(bf16, p.cfg.head_dim, group_of(p.cfg), paged);
   if (fn == nullptr) return COMEM_ERR_UNSUPPORTED;
   dim3 grid(static_cast<unsigned>(splits), static_cast<unsigned>(p.cfg.num_kv_heads),
@@ -273,7 +282,9 @@ void fill_common(const comem_decode_attn_plan& p, comem::AttnParams& a, const vo
   a.group = group_of(p.cfg);
   a.chunk = static_cast<int32_t>(chunk);
   a.num_splits = static_cast<int32_t>(splits);
-  a.scale_log2 = p.cfg.scale * 1.4426950408889634f;
+  // An FP8 cache's K scale multiplies every score; its V scale every output.
+  a.scale_log2 = p.cfg.scale * (is_fp8(p.cfg) ? p.cfg.k_scale : 1.f) * 1.4426950408889634f;
+  a.out_scale = is_fp8(p.cfg) ? p.cfg.v_scale : 1.f;
   a.queue_slot = p.cfg.max_batch * p.cfg.num_kv_heads;
   if (splits > 1 || queue) {
     char* ws = static_cast<char*>(workspace);

@@ -57,6 +57,7 @@ struct AttnParams {
   const char* new_k;   // fused append: new rows [B, Hkv, D], or nullptr for attention only
   const char* new_v;
   int64_t num_pages;   // paged layout: pool size (bounds the fused append's store)
+  float out_scale;     // multiplies every output (the V scale of an FP8 cache, else 1)
 };
 
 // Per-wave partial state handed from the token loop to the finalize step.
@@ -203,7 +204,9 @@ __device__ void finalize_split(const AttnParams& p, const WaveState<D>& ws, int 
     const float4 on = make_float4(st.acc.x * inv, st.acc.y * inv, st.acc.z * inv, st.acc.w * inv);
     const float lse2 = live ? st.m + log2f(st.wsum) : -INFINITY;
     if (single) {
-      *reinterpret_cast<float4*>(p.out + static_cast<int64_t>(head0 + h) * D + d0) = on;
+      const float os = p.out_scale;
+      *reinterpret_cast<float4*>(p.out + static_cast<int64_t>(head0 + h) * D + d0) =
+          make_float4(on.x * os, on.y * os, on.z * os, on.w * os);
       if (d0 == 0 && p.lse != nullptr) p.lse[head0 + h] = live ? lse2 * kLn2 : -INFINITY;
     } else {
       store4_coherent(ro, ((j * G + h) * D + d0) * 4, on);
@@ -252,7 +255,7 @@ __device__ void finalize_split(const AttnParams& p, const WaveState<D>& ws, int 
       for (int i = 0; i < kMergeBatch; ++i) st.add(s0 + i * tps < nsplit_b ? l2[i] : -INFINITY, 1.f, o[i]);
     }
     if (tps == 1) {
-      const float inv = 1.f / st.wsum;
+      const float inv = p.out_scale / st.wsum;
       *reinterpret_cast<float4*>(p.out + static_cast<int64_t>(head0 + h) * D + d0) =
           make_float4(st.acc.x * inv, st.acc.y * inv, st.acc.z * inv, st.acc.w * inv);
       if (d0 == 0 && p.lse != nullptr) p.lse[head0 + h] = (st.m + log2f(st.wsum)) * kLn2;
@@ -270,7 +273,7 @@ __device__ void finalize_split(const AttnParams& p, const WaveState<D>& ws, int 
     const int d0 = slot * 4 - h * D;
     MergeState st;
     for (int i = 0; i < tps; ++i) st.add(sm_m[tid + i], sm_w[tid + i], sm_acc[tid + i]);
-    const float inv = 1.f / st.wsum;
+    const float inv = p.out_scale / st.wsum;
     *reinterpret_cast<float4*>(p.out + static_cast<int64_t>(head0 + h) * D + d0) =
         make_float4(st.acc.x * inv, st.acc.y * inv, st.acc.z * inv, st.acc.w * inv);
     if (d0 == 0 && p.lse != nullptr) p.lse[head0 + h] = (st.m + log2f(st.wsum)) * kLn2;

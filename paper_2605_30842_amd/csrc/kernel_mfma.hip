@@ -29,6 +29,14 @@
 // The reduction index of an MFMA is a dummy index, so any consistent
 // assignment of (lane, element) to tokens or head_dim positions is valid as
 // long as A and B use the same one, which they do by construction above.
+//
+// FP8 caches (OCP E4M3 codes with a per-tensor scale) use the same tiles at
+// one byte per element and widen the codes to bf16 in registers before the
+// matrix-core steps (exact: every E4M3 value is a bf16 value). The scales
+// are folded into the score scale (K) and the final output (V). For the QK
+// step a lane's K slice is then its D / 4 consecutive codes (head_dim
+// (D / 4) g onward, 16 per 16-byte load): k-block kb is head_dim
+// (D / 4) g + 8 kb .. + 8, and the Q operand follows the same assignment.
 #include "attn_common.h"
 
 namespace comem {
@@ -73,6 +81,70 @@ struct Tile {
 
 __device__ inline bf16x8 as_bf16x8(u32x4 x) { return __builtin_bit_cast(bf16x8, x); }
 
+// The V slice of a row in an FP8 cache: NT one-byte codes.
+template <int D>
+struct VRow8;
+template <>
+struct VRow8<128> {
+  u32x2 w;
+  __device__ void load(__amdgpu_buffer_rsrc_t r, uint32_t voff, int soff) {
+    w = __builtin_bit_cast(u32x2, __builtin_amdgcn_raw_buffer_load_b64(r, voff, soff, kStreaming));
+  }
+};
+template <>
+struct VRow8<64> {
+  uint32_t w;
+  __device__ void load(__amdgpu_buffer_rsrc_t r, uint32_t voff, int soff) {
+    w = __builtin_amdgcn_raw_buffer_load_b32(r, voff, soff, kStreaming);
+  }
+};
+
+template <int D>
+struct Tile8 {
+  u32x4 k[2][D / 64];  // [sub-tile][16 codes]: the lane's D / 4 codes of its K row
+  VRow8<D> v[2][4];
+};
+
+template <int D, bool FP8>
+struct TileOf {
+  using type = Tile<D>;
+};
+template <int D>
+struct TileOf<D, true> {
+  using type = Tile8<D>;
+};
+
+// Two E4M3 codes (bytes 0-1, or 2-3 with HIGH) of w as a bf16 pair, low element first.
+template <bool HIGH>
+__device__ inline uint32_t e4m3_pair_to_bf16(uint32_t w) {
+  return __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(w, 1.0f, HIGH));
+}
+
+// Widen an FP8 tile to the bf16 tile the matrix-core steps read.
+template <int D>
+__device__ inline void widen_tile(const Tile8<D>& R, Tile<D>& T) {
+  constexpr int KB = D / 32;
+#pragma unroll
+  for (int s = 0; s < 2; ++s) {
+#pragma unroll
+    for (int kb = 0; kb < KB; ++kb) {
+      const uint32_t w0 = R.k[s][kb >> 1][2 * (kb & 1)], w1 = R.k[s][kb >> 1][2 * (kb & 1) + 1];
+      T.k[s][kb] = u32x4{e4m3_pair_to_bf16<false>(w0), e4m3_pair_to_bf16<true>(w0), e4m3_pair_to_bf16<false>(w1),
+                         e4m3_pair_to_bf16<true>(w1)};
+    }
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      if constexpr (D == 128) {
+        const u32x2 w = R.v[s][r].w;
+        T.v[s][r].w = u32x4{e4m3_pair_to_bf16<false>(w[0]), e4m3_pair_to_bf16<true>(w[0]),
+                            e4m3_pair_to_bf16<false>(w[1]), e4m3_pair_to_bf16<true>(w[1])};
+      } else {
+        T.v[s][r].w = u32x2{e4m3_pair_to_bf16<false>(R.v[s][r].w), e4m3_pair_to_bf16<true>(R.v[s][r].w)};
+      }
+    }
+  }
+}
+
 // Page lookups of one split go through LDS: the workgroup copies the split's
 // block-table entries there once, so the token loop never waits on them.
 constexpr int kMaxSplitPages = 2048;
@@ -81,8 +153,10 @@ constexpr int kMaxQueueBatch = 4096;
 
 enum class Layout { kContig, kPaged, kPagedFine };
 
-template <int D, Layout LAYOUT>
+template <int D, Layout LAYOUT, bool FP8>
 struct Loader {
+  using TileT = typename TileOf<D, FP8>::type;
+  static constexpr int kElemBytes = FP8 ? 1 : 2;
   const char* kbase;  // K of this (b, hk): contiguous layout already offset to the sequence start
   const char* vbase;
   const int32_t* sm_pages;  // LDS copy of the split's block-table entries (paged layouts)
@@ -92,8 +166,8 @@ struct Loader {
   int page_shift, page_mask;
   int t_end;
   int c, g;
-  uint32_t koff;  // c * stride_token + 16 g
-  uint32_t voff;  // 4 g * stride_token + 2 * NT * c
+  uint32_t koff;  // c * stride_token + 16 g (FP8: + (D / 4) g)
+  uint32_t voff;  // 4 g * stride_token + (NT * c elements)
 
   // Byte offset of token t from the base; uniform across the wave when t is.
   __device__ int64_t token_offset(int t) const {
@@ -112,9 +186,9 @@ struct Loader {
   // touching memory should an offset ever fall outside them. With `repeat`
   // the call only keeps the load count of the pipeline steady: it re-reads
   // the tile's K rows (still cached) into both halves and its data is unused.
-  __device__ void load_full(Tile<D>& T, int t0, bool repeat) const {
+  __device__ void load_full(TileT& T, int t0, bool repeat) const {
     constexpr int KB = D / 32;
-    const int extent = static_cast<int>(15 * stride_token + 2 * D);
+    const int extent = static_cast<int>(15 * stride_token + kElemBytes * D);
 #pragma unroll
     for (int s = 0; s < 2; ++s) {
       const int64_t base = uniform_i64(token_offset(t0 + 16 * s));
@@ -122,9 +196,15 @@ struct Loader {
           __builtin_amdgcn_make_buffer_rsrc(const_cast<char*>(kbase + base), 0, extent, kBufferConfig);
       const __amdgpu_buffer_rsrc_t rv = __builtin_amdgcn_make_buffer_rsrc(
           const_cast<char*>((repeat ? kbase : vbase) + base), 0, extent, kBufferConfig);
+      if constexpr (FP8) {
 #pragma unroll
-      for (int kk = 0; kk < KB; ++kk)
-        T.k[s][kk] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rk, koff + 64 * kk, 0, 0));
+        for (int i = 0; i < D / 64; ++i)
+          T.k[s][i] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rk, koff + 16 * i, 0, 0));
+      } else {
+#pragma unroll
+        for (int kk = 0; kk < KB; ++kk)
+          T.k[s][kk] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rk, koff + 64 * kk, 0, 0));
+      }
 #pragma unroll
       for (int r = 0; r < 4; ++r) T.v[s][r].load(rv, voff, static_cast<int>(r * stride_token));
     }
@@ -132,14 +212,19 @@ struct Loader {
 
   // Any tile: per-lane rows; tokens past the end are clamped to the last
   // valid row (their weight is zero), so no byte outside a context is read.
-  __device__ void load_any(Tile<D>& T, int t0) const {
+  __device__ void load_any(TileT& T, int t0) const {
     constexpr int KB = D / 32;
-    constexpr int VBYTES = D / 8;
+    constexpr int VBYTES = kElemBytes * D / 16;
 #pragma unroll
     for (int s = 0; s < 2; ++s) {
-      const char* kr = kbase + token_offset(min(t0 + 16 * s + c, t_end - 1)) + 16 * g;
+      const char* kr = kbase + token_offset(min(t0 + 16 * s + c, t_end - 1)) + (FP8 ? (D / 4) * g : 16 * g);
+      if constexpr (FP8) {
 #pragma unroll
-      for (int kk = 0; kk < KB; ++kk) T.k[s][kk] = *reinterpret_cast<const u32x4*>(kr + 64 * kk);
+        for (int i = 0; i < D / 64; ++i) T.k[s][i] = *reinterpret_cast<const u32x4*>(kr + 16 * i);
+      } else {
+#pragma unroll
+        for (int kk = 0; kk < KB; ++kk) T.k[s][kk] = *reinterpret_cast<const u32x4*>(kr + 64 * kk);
+      }
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const char* vr = vbase + token_offset(min(t0 + 16 * s + 4 * g + r, t_end - 1)) + VBYTES * c;
@@ -223,6 +308,20 @@ __device__ inline void compute_tile(const Tile<D>& T, int t0, int t_end, int c, 
   }
 }
 
+// compute_tile on a tile as loaded (FP8 tiles are widened first).
+template <int D, bool FP8>
+__device__ inline void compute_loaded(const typename TileOf<D, FP8>::type& T, int t0, int t_end, int c, int g,
+                                      const bf16x8 (&qop)[D / 32], float scale_log2, float& m_run, float& l_run,
+                                      f32x4 (&acc)[D / 16]) {
+  if constexpr (FP8) {
+    Tile<D> W;
+    widen_tile<D>(T, W);
+    compute_tile<D>(W, t0, t_end, c, g, qop, scale_log2, m_run, l_run, acc);
+  } else {
+    compute_tile<D>(T, t0, t_end, c, g, qop, scale_log2, m_run, l_run, acc);
+  }
+}
+
 // ctx_lens[b] and, for the contiguous layout, seq_start[b]: both loads are
 // issued before either value is used (the empty asm consumes both at once),
 // so they share one memory round trip.
@@ -252,9 +351,10 @@ struct SplitSmem {
 // With next_item set (work-queue form), thread 0 takes the workgroup's next
 // item from the queue once the token loop is done: issued earlier, the queue
 // atomic would sit ahead of the tile loads in the in-order memory counter.
-template <int D, Layout LAYOUT>
+template <int D, Layout LAYOUT, bool FP8>
 __device__ void attend_split(const AttnParams& p, SplitSmem<D, LAYOUT>& sm, int b, int hk, int j, int L,
                              int64_t seq_row, int* next_item) {
+  using TileT = typename TileOf<D, FP8>::type;
   constexpr int KB = D / 32;
   constexpr int NT = D / 16;
   const int nsplit_b = L > 0 ? 1 + (L - 1) / p.chunk : 1;
@@ -265,7 +365,7 @@ __device__ void attend_split(const AttnParams& p, SplitSmem<D, LAYOUT>& sm, int 
   const int c = lane & 15, g = lane >> 4;
   const int G = p.group;
 
-  Loader<D, LAYOUT> ld;
+  Loader<D, LAYOUT, FP8> ld;
   ld.kbase = p.k + hk * p.stride_head;
   ld.vbase = p.v + hk * p.stride_head;
   if constexpr (LAYOUT == Layout::kContig) {
@@ -289,17 +389,18 @@ __device__ void attend_split(const AttnParams& p, SplitSmem<D, LAYOUT>& sm, int 
   ld.t_end = t_end;
   ld.c = c;
   ld.g = g;
-  ld.koff = static_cast<uint32_t>(c * p.stride_token + 16 * g);
-  ld.voff = static_cast<uint32_t>(4 * g * p.stride_token + 2 * NT * c);
+  ld.koff = static_cast<uint32_t>(c * p.stride_token + (FP8 ? (D / 4) * g : 16 * g));
+  ld.voff = static_cast<uint32_t>(4 * g * p.stride_token + (FP8 ? NT : 2 * NT) * c);
 
-  // Q operand: head c of the group (zero columns past G), slice 32kb + 8g.
+  // Q operand: head c of the group (zero columns past G), slice 32kb + 8g
+  // (FP8 caches: (D / 4) g + 8 kb, the slice the lane's K codes cover).
   bf16x8 qop[KB];
   {
     const char* qrow = p.q + (static_cast<int64_t>(b) * p.num_q_heads + hk * G + c) * D * 2;
 #pragma unroll
     for (int kk = 0; kk < KB; ++kk) {
       u32x4 qv = u32x4{0u, 0u, 0u, 0u};
-      if (c < G) qv = *reinterpret_cast<const u32x4*>(qrow + 64 * kk + 16 * g);
+      if (c < G) qv = *reinterpret_cast<const u32x4*>(qrow + (FP8 ? (D / 2) * g + 16 * kk : 64 * kk + 16 * g));
       qop[kk] = as_bf16x8(qv);
     }
   }
@@ -320,7 +421,7 @@ __device__ void attend_split(const AttnParams& p, SplitSmem<D, LAYOUT>& sm, int 
     } else {
       row = checked_page_row(p, sm.pages[((L - 1) - ld.page_first) >> p.page_shift], L - 1);
     }
-    store_new_token(p, b, hk, row, D / 8, lane);
+    store_new_token(p, b, hk, row, FP8 ? D / 16 : D / 8, lane);
   }
   int ti = w;
   if constexpr (LAYOUT != Layout::kPagedFine) {
@@ -329,34 +430,34 @@ __device__ void attend_split(const AttnParams& p, SplitSmem<D, LAYOUT>& sm, int 
     // it re-reads cached K rows of the current one) and pinned ahead of the
     // compute, so the compiler waits for exactly the older tile's loads.
     if (ti < nfull) {
-      Tile<D> A, B;
+      TileT A, B;
       ld.load_full(A, t_begin + 32 * ti, false);
       for (;;) {
         int nx = ti + kWaves;
         ld.load_full(B, t_begin + 32 * (nx < nfull ? nx : ti), nx >= nfull);
         __builtin_amdgcn_sched_barrier(0);
-        compute_tile<D>(A, t_begin + 32 * ti, t_end, c, g, qop, p.scale_log2, m_run, l_run, acc);
+        compute_loaded<D, FP8>(A, t_begin + 32 * ti, t_end, c, g, qop, p.scale_log2, m_run, l_run, acc);
         if (nx >= nfull) break;
         ti = nx;
         nx = ti + kWaves;
         ld.load_full(A, t_begin + 32 * (nx < nfull ? nx : ti), nx >= nfull);
         __builtin_amdgcn_sched_barrier(0);
-        compute_tile<D>(B, t_begin + 32 * ti, t_end, c, g, qop, p.scale_log2, m_run, l_run, acc);
+        compute_loaded<D, FP8>(B, t_begin + 32 * ti, t_end, c, g, qop, p.scale_log2, m_run, l_run, acc);
         if (nx >= nfull) break;
         ti = nx;
       }
     }
     ti = nfull;  // the partial tile, if any, belongs to wave nfull % kWaves
     if (ti < ntiles && (ti % kWaves) == w) {
-      Tile<D> A;
+      TileT A;
       ld.load_any(A, t_begin + 32 * ti);
-      compute_tile<D>(A, t_begin + 32 * ti, t_end, c, g, qop, p.scale_log2, m_run, l_run, acc);
+      compute_loaded<D, FP8>(A, t_begin + 32 * ti, t_end, c, g, qop, p.scale_log2, m_run, l_run, acc);
     }
   } else {
     for (; ti < ntiles; ti += kWaves) {
-      Tile<D> A;
+      TileT A;
       ld.load_any(A, t_begin + 32 * ti);
-      compute_tile<D>(A, t_begin + 32 * ti, t_end, c, g, qop, p.scale_log2, m_run, l_run, acc);
+      compute_loaded<D, FP8>(A, t_begin + 32 * ti, t_end, c, g, qop, p.scale_log2, m_run, l_run, acc);
     }
   }
 
@@ -383,7 +484,7 @@ __device__ void attend_split(const AttnParams& p, SplitSmem<D, LAYOUT>& sm, int 
 }
 
 // One workgroup per (split, KV head, sequence); splits past a sequence's end exit.
-template <int D, Layout LAYOUT>
+template <int D, Layout LAYOUT, bool FP8>
 __global__ __launch_bounds__(kThreads, 2) void decode_mfma_kernel(const AttnParams p) {
   const int j = blockIdx.x, hk = blockIdx.y, b = blockIdx.z;
   int L;
@@ -392,7 +493,7 @@ __global__ __launch_bounds__(kThreads, 2) void decode_mfma_kernel(const AttnPara
   const int nsplit_b = L > 0 ? 1 + (L - 1) / p.chunk : 1;
   if (j >= nsplit_b) return;
   __shared__ SplitSmem<D, LAYOUT> sm;
-  attend_split<D, LAYOUT>(p, sm, b, hk, j, L, seq_row, nullptr);
+  attend_split<D, LAYOUT, FP8>(p, sm, b, hk, j, L, seq_row, nullptr);
 }
 
 // Persistent workgroups that take work items from a queue. Item i stands for
@@ -403,7 +504,7 @@ __global__ __launch_bounds__(kThreads, 2) void decode_mfma_kernel(const AttnPara
 // count of finished workgroups live next to the tickets and return to zero
 // when the last workgroup leaves. Faster XCDs and compute units simply take
 // more items, and ragged batches need no empty workgroups.
-template <int D, Layout LAYOUT>
+template <int D, Layout LAYOUT, bool FP8>
 __global__ __launch_bounds__(kThreads, 2) void decode_mfma_queue_kernel(const AttnParams p, int batch) {
   __shared__ SplitSmem<D, LAYOUT> sm;
   __shared__ int sm_first[kMaxQueueBatch + 1];  // first split index of each sequence; last = total
@@ -453,7 +554,7 @@ __global__ __launch_bounds__(kThreads, 2) void decode_mfma_queue_kernel(const At
     int L;
     int64_t seq_row;
     load_sequence<LAYOUT>(p, b, L, seq_row);
-    attend_split<D, LAYOUT>(p, sm, b, hk, split_index - sm_first[b], L, seq_row, queued ? &sm_next : nullptr);
+    attend_split<D, LAYOUT, FP8>(p, sm, b, hk, split_index - sm_first[b], L, seq_row, queued ? &sm_next : nullptr);
     __syncthreads();
     item = queued ? sm_next : total;
     __syncthreads();
@@ -469,28 +570,30 @@ __global__ __launch_bounds__(kThreads, 2) void decode_mfma_queue_kernel(const At
 using KernelFn = void (*)(AttnParams);
 using QueueKernelFn = void (*)(AttnParams, int);
 
-template <int D>
+template <int D, bool FP8>
 KernelFn pick_layout(bool paged, int page_size) {
-  if (!paged) return decode_mfma_kernel<D, Layout::kContig>;
-  return page_size >= 16 ? decode_mfma_kernel<D, Layout::kPaged> : decode_mfma_kernel<D, Layout::kPagedFine>;
+  if (!paged) return decode_mfma_kernel<D, Layout::kContig, FP8>;
+  return page_size >= 16 ? decode_mfma_kernel<D, Layout::kPaged, FP8> : decode_mfma_kernel<D, Layout::kPagedFine, FP8>;
 }
 
-template <int D>
+template <int D, bool FP8>
 QueueKernelFn pick_queue_layout(bool paged, int page_size) {
-  if (!paged) return decode_mfma_queue_kernel<D, Layout::kContig>;
-  return page_size >= 16 ? decode_mfma_queue_kernel<D, Layout::kPaged>
-                         : decode_mfma_queue_kernel<D, Layout::kPagedFine>;
+  if (!paged) return decode_mfma_queue_kernel<D, Layout::kContig, FP8>;
+  return page_size >= 16 ? decode_mfma_queue_kernel<D, Layout::kPaged, FP8>
+                         : decode_mfma_queue_kernel<D, Layout::kPagedFine, FP8>;
 }
 
-KernelFn select_mfma_kernel(int head_dim, bool paged, int page_size) {
-  if (head_dim == 128) return pick_layout<128>(paged, page_size);
-  if (head_dim == 64) return pick_layout<64>(paged, page_size);
+KernelFn select_mfma_kernel(int head_dim, bool paged, int page_size, bool fp8) {
+  if (head_dim == 128) return fp8 ? pick_layout<128, true>(paged, page_size) : pick_layout<128, false>(paged, page_size);
+  if (head_dim == 64) return fp8 ? pick_layout<64, true>(paged, page_size) : pick_layout<64, false>(paged, page_size);
   return nullptr;
 }
 
-QueueKernelFn select_mfma_queue_kernel(int head_dim, bool paged, int page_size) {
-  if (head_dim == 128) return pick_queue_layout<128>(paged, page_size);
-  if (head_dim == 64) return pick_queue_layout<64>(paged, page_size);
+QueueKernelFn select_mfma_queue_kernel(int head_dim, bool paged, int page_size, bool fp8) {
+  if (head_dim == 128)
+    return fp8 ? pick_queue_layout<128, true>(paged, page_size) : pick_queue_layout<128, false>(paged, page_size);
+  if (head_dim == 64)
+    return fp8 ? pick_queue_layout<64, true>(paged, page_size) : pick_queue_layout<64, false>(paged, page_size);
   return nullptr;
 }
 

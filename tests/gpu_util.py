@@ -18,6 +18,7 @@ def say(*a):
 
 
 def to_torch(arr, dtype, device):
+    """bf16 bit patterns -> a bfloat16 tensor; fp8 codes stay uint8; other arrays as they are."""
     import torch
 
     if dtype == "bf16" and arr.dtype == np.uint16:
@@ -34,7 +35,7 @@ class DeviceWorkload:
         s = w.spec
         self.w = w
         self.spec = s
-        self.q = to_torch(w.q, s.dtype, device)
+        self.q = to_torch(w.q, s.q_dtype, device)
         self.ctx_lens = torch.from_numpy(w.ctx_lens.astype(np.int32)).to(device)
         if s.layout == "paged":
             self.k = to_torch(w.k_pages, s.dtype, device)
@@ -49,9 +50,10 @@ class DeviceWorkload:
 def make_op(spec, chunk=0, variant="auto", max_batch=None, max_ctx_len=None):
     from paper_2605_30842_amd.binding import DecodeAttention
 
+    scales = dict(k_scale=spec.k_scale, v_scale=spec.v_scale) if spec.dtype == "fp8" else {}
     return DecodeAttention(spec.num_q_heads, spec.num_kv_heads, spec.head_dim, spec.dtype, float(spec.scale),
                            max_batch or spec.batch, max_ctx_len or spec.max_ctx_len, chunk_tokens=chunk,
-                           variant=variant)
+                           variant=variant, **scales)
 
 
 def run(dw: DeviceWorkload, op, want_lse=True, max_ctx_len=None):
@@ -71,7 +73,7 @@ def run(dw: DeviceWorkload, op, want_lse=True, max_ctx_len=None):
 
 
 def check(out, lse, ref_out, ref_lse, dtype, what=""):
-    """Assert the official gate (and, for bf16, the internal diagnostic gate); return max |err|."""
+    """Assert the official gate (and, for bf16 and fp8 caches, the internal diagnostic gate); return max |err|."""
     out = np.asarray(out, dtype=np.float64)
     ref_out = np.asarray(ref_out, dtype=np.float64)
     assert out.shape == ref_out.shape, what

@@ -48,7 +48,7 @@ def test_probe_library_exports_its_header():
 
 def _cfg(**kw):
     base = dict(num_q_heads=32, num_kv_heads=8, head_dim=128, dtype=B.BF16, scale=0.088, max_batch=4,
-                max_ctx_len=4096, chunk_tokens=0, variant=B.VARIANT_AUTO)
+                max_ctx_len=4096, chunk_tokens=0, variant=B.VARIANT_AUTO, k_scale=1.0, v_scale=1.0)
     base.update(kw)
     return B.Config(**base)
 
@@ -355,5 +355,34 @@ def test_prefill_needs_bf16():
     p, _ = B.comem_decode_attn_init(_cfg(dtype=B.F32), B.NO_DEVICE)
     try:
         assert B.load_library().comem_prefill_attn(*_prefill_args(p).values()) == B.ERR_UNSUPPORTED
+    finally:
+        B.comem_decode_attn_destroy(p)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(dtype=B.FP8_E4M3), B.OK),
+    (dict(dtype=B.FP8_E4M3, variant=B.VARIANT_MFMA), B.OK),
+    (dict(dtype=B.FP8_E4M3, variant=B.VARIANT_MFMA_GRID), B.OK),
+    (dict(dtype=B.FP8_E4M3, variant=B.VARIANT_VALU), B.ERR_UNSUPPORTED),
+    (dict(dtype=B.FP8_E4M3, k_scale=0.0), B.ERR_INVALID_SHAPE),
+    (dict(dtype=B.FP8_E4M3, v_scale=-1.0), B.ERR_INVALID_SHAPE),
+    (dict(dtype=B.FP8_E4M3, k_scale=float("inf")), B.ERR_INVALID_SHAPE),
+    (dict(dtype=B.FP8_E4M3, v_scale=float("nan")), B.ERR_INVALID_SHAPE),
+    (dict(dtype=B.BF16, k_scale=0.0, v_scale=0.0), B.OK),  # scales are only read for FP8 caches
+    (dict(dtype=3), B.ERR_UNSUPPORTED),
+])
+def test_fp8_config_validation(kw, status):
+    assert _status_init(_cfg(**kw)) == status
+
+
+def test_fp8_strides_are_bytes():
+    """An FP8 cache row of 8 heads x 128 codes is 1024 bytes: strides are counted in elements = bytes."""
+    p, ws = B.comem_decode_attn_init(_cfg(dtype=B.FP8_E4M3), B.NO_DEVICE)
+    try:
+        lib = B.load_library()
+        assert lib.comem_decode_attn(*_contig_args(p, ws).values()) == B.ERR_NO_DEVICE
+        assert lib.comem_decode_attn(*_contig_args(p, ws, stride_token=8 * 128 + 8).values()) == B.ERR_MISALIGNED
+        assert lib.comem_decode_attn(*_contig_args(p, ws, stride_token=8 * 128 + 16).values()) == B.ERR_NO_DEVICE
+        assert lib.comem_prefill_attn(*_prefill_args(p).values()) == B.ERR_UNSUPPORTED
     finally:
         B.comem_decode_attn_destroy(p)
