@@ -46,10 +46,11 @@
 // maximum exceeds it by more than 2^8 in probability, so the accumulators are
 // rescaled rarely and every probability stays below 2^8.
 //
-// K and V tiles go global -> registers -> LDS, one tile ahead of the compute,
-// into two LDS buffers. Global loads use buffer descriptors whose base and
-// size are uniform per tile (or per 16-row group of a page), so addresses are
-// scalar arithmetic and rows past the keys a block needs read as zero. In
+// K and V tiles go from global memory straight into LDS (buffer loads with an
+// LDS destination), one tile ahead of the compute, into two LDS buffers. The
+// descriptors' base and size are uniform per 16-row group (one page when
+// pages hold 16 rows or more), so addresses are scalar arithmetic and rows
+// past the keys a block needs arrive as zeros. In
 // LDS, 16-byte chunk c of row r sits at chunk c ^ f(r), with f chosen so that
 // the K reads (one chunk of 8 or 16 consecutive rows), the V transpose reads
 // (4 chunks of 4 consecutive rows) and the stores are all free of bank
@@ -70,12 +71,14 @@ typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
 
 constexpr float kLazyMax = 8.f;  // log2 of the largest probability the lazy maximum allows
 
+// One LDS buffer: a K tile and a V tile. The kernel keeps two as separate
+// objects, so the compiler can tell the loads streaming into one from the
+// reads of the other and does not wait for them.
 template <int D>
-struct PrefillSmem {
-  static constexpr int kRowBytes = D * 2;
-  static constexpr int kTileBytes = kPrefillTileKeys * kRowBytes;
-  static constexpr int kBufBytes = 2 * kTileBytes;  // K then V of one buffer
-  char buf[2][2][kTileBytes];                       // [buffer][K, V]
+struct TileBuf {
+  static constexpr int kTileBytes = kPrefillTileKeys * D * 2;
+  char k[kTileBytes];
+  char v[kTileBytes];
 };
 
 // Chunk swizzle of a row (depends on its low 4 bits only).
@@ -93,23 +96,44 @@ __device__ inline int lds_offset(int r, int c) {
 
 enum class PLayout { kContig, kPaged, kPagedFine };
 
-// One thread's share of a K/V tile: chunk c of rows row0 + RSTEP u.
+typedef __attribute__((address_space(3))) void lds_void;
+
+// Wave w loads rows 16 w .. 16 w + 15 of every K and V tile straight into
+// LDS (buffer loads with an LDS destination, no registers in between).
+// Instruction u writes 1 KiB from row 16 w + RPI u on: lane l the 16 bytes at
+// LDS offset 16 l, i.e. physical chunk l % CH of row 16 w + RPI u + l / CH,
+// which holds logical chunk (l % CH) ^ f(row). The swizzle depends on the
+// row's low 4 bits only, so the lane offsets are the same for every tile and
+// group. Rows past the keys a block needs are outside the descriptor and
+// arrive as zeros (checked on the device); a zero V row times a zero weight
+// adds nothing. Small pages (a 16-row group spanning pages) take per-lane
+// addresses, with rows past the needed keys clamped to the last one.
 template <int D, PLayout LAYOUT>
 struct TileLoader {
-  static constexpr int CH = D / 8;                    // 16-byte chunks per row
-  static constexpr int RSTEP = kPrefillThreads / CH;  // rows between a thread's chunks
-  static constexpr int NU = kPrefillTileKeys / RSTEP;  // chunks per thread per tensor
+  static constexpr int CH = D / 8;      // 16-byte chunks per row
+  static constexpr int RPI = 64 / CH;   // rows per wave instruction (1 KiB)
+  static constexpr int NI = 16 / RPI;   // instructions per 16-row group
   const char* kbase;  // K of this KV head (contiguous: at the sequence's first row)
   const char* vbase;
   const int32_t* bt_row;  // block-table row of the sequence (paged)
   int64_t stride_token;
   int64_t stride_page;
   int page_shift, page_mask;
-  int kend;  // keys [0, kend) are read; later rows read as zero (or repeat key kend - 1)
-  int c, row0;
-  uint32_t voff;  // row0 * stride_token + 16 c
-  u32x4 kreg[NU], vreg[NU];
-  int32_t page[NU];  // kPaged: one entry per group of RSTEP rows; kPagedFine: per row
+  int kend;  // keys [0, kend) are needed
+  int w, lane;
+  uint32_t voff[NI];     // lane offset of instruction u within a 16-row group
+  int32_t page;          // kPaged: entry of this wave's group in the next tile to load (uniform)
+  int32_t fine_page[NI]; // kPagedFine: per-lane entries for the next tile to load
+
+  __device__ void init(int wave, int ln) {
+    w = wave;
+    lane = ln;
+#pragma unroll
+    for (int u = 0; u < NI; ++u) {
+      const int r = RPI * u + lane / CH;
+      voff[u] = static_cast<uint32_t>(r * stride_token + 16 * ((lane % CH) ^ swizzle<D>(r)));
+    }
+  }
 
   // Buffer descriptor over `rows` rows from `base`; never more than 4 GiB.
   __device__ __amdgpu_buffer_rsrc_t rsrc(const char* base, int rows) const {
@@ -118,65 +142,53 @@ struct TileLoader {
     return __builtin_amdgcn_make_buffer_rsrc(const_cast<char*>(base), 0, static_cast<int>(n), kBufferConfig);
   }
 
-  __device__ int key(int t0, int u) const { return min(t0 + row0 + u * RSTEP, kend - 1); }
+  __device__ int fine_key(int t0, int u) const { return min(t0 + 16 * w + RPI * u + lane / CH, kend - 1); }
 
   __device__ void fetch_pages(int t0) {
     if constexpr (LAYOUT == PLayout::kPaged) {
-#pragma unroll
-      for (int u = 0; u < NU; ++u) {
-        const int g0 = t0 + u * RSTEP;
-        page[u] = g0 < kend ? bt_row[g0 >> page_shift] : 0;
-      }
+      const int g0 = t0 + 16 * w;
+      page = g0 < kend ? bt_row[g0 >> page_shift] : 0;
     } else if constexpr (LAYOUT == PLayout::kPagedFine) {
 #pragma unroll
-      for (int u = 0; u < NU; ++u) page[u] = bt_row[key(t0, u) >> page_shift];
+      for (int u = 0; u < NI; ++u) fine_page[u] = bt_row[fine_key(t0, u) >> page_shift];
     }
   }
 
-  __device__ void load(int t0) {
-    if constexpr (LAYOUT == PLayout::kContig) {
-      const int64_t base = static_cast<int64_t>(t0) * stride_token;
-      const int rows = min(kend - t0, kPrefillTileKeys);
-      const __amdgpu_buffer_rsrc_t rk = rsrc(kbase + base, rows), rv = rsrc(vbase + base, rows);
+  __device__ void load(TileBuf<D>& tb, int t0) const {
+    constexpr int RB = D * 2;
+    char* kd = tb.k + 16 * w * RB;
+    char* vd = tb.v + 16 * w * RB;
+    if constexpr (LAYOUT == PLayout::kPagedFine) {
 #pragma unroll
-      for (int u = 0; u < NU; ++u) {
-        const int so = static_cast<int>(static_cast<uint32_t>(u * RSTEP * stride_token));
-        kreg[u] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rk, voff, so, 0));
-        vreg[u] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rv, voff, so, 0));
-      }
-    } else if constexpr (LAYOUT == PLayout::kPaged) {
-      // A group of RSTEP rows lies in one page (page_size >= RSTEP).
-#pragma unroll
-      for (int u = 0; u < NU; ++u) {
-        const int g0 = t0 + u * RSTEP;
-        const int rows = max(0, min(kend - g0, RSTEP));
-        const int64_t base =
-            static_cast<int64_t>(page[u]) * stride_page + static_cast<int64_t>(g0 & page_mask) * stride_token;
-        const __amdgpu_buffer_rsrc_t rk = rsrc(kbase + base, rows), rv = rsrc(vbase + base, rows);
-        kreg[u] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rk, voff, 0, 0));
-        vreg[u] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rv, voff, 0, 0));
+      for (int u = 0; u < NI; ++u) {
+        const int t = fine_key(t0, u);
+        const int64_t off = static_cast<int64_t>(fine_page[u]) * stride_page +
+                            static_cast<int64_t>(t & page_mask) * stride_token + 16 * ((lane % CH) ^ swizzle<D>(RPI * u + lane / CH));
+        __builtin_amdgcn_global_load_lds(kbase + off, (lds_void*)(kd + u * RPI * RB), 16, 0, 0);
+        __builtin_amdgcn_global_load_lds(vbase + off, (lds_void*)(vd + u * RPI * RB), 16, 0, 0);
       }
     } else {
-#pragma unroll
-      for (int u = 0; u < NU; ++u) {
-        const int t = key(t0, u);
-        const int64_t off = static_cast<int64_t>(page[u]) * stride_page +
-                            static_cast<int64_t>(t & page_mask) * stride_token + c * 16;
-        kreg[u] = *reinterpret_cast<const u32x4*>(kbase + off);
-        vreg[u] = *reinterpret_cast<const u32x4*>(vbase + off);
+      const int g0 = t0 + 16 * w;
+      const int rows = max(0, min(kend - g0, 16));
+      int64_t base;
+      if constexpr (LAYOUT == PLayout::kContig) {
+        base = static_cast<int64_t>(g0) * stride_token;
+      } else {
+        base = static_cast<int64_t>(page) * stride_page + static_cast<int64_t>(g0 & page_mask) * stride_token;
       }
-    }
-  }
-
-  __device__ void store(PrefillSmem<D>& sm, int b) const {
+      const __amdgpu_buffer_rsrc_t rk = rsrc(kbase + base, rows), rv = rsrc(vbase + base, rows);
 #pragma unroll
-    for (int u = 0; u < NU; ++u) {
-      const int off = lds_offset<D>(row0 + u * RSTEP, c);
-      *reinterpret_cast<u32x4*>(sm.buf[b][0] + off) = kreg[u];
-      *reinterpret_cast<u32x4*>(sm.buf[b][1] + off) = vreg[u];
+      for (int u = 0; u < NI; ++u) {
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rk, (lds_void*)(kd + u * RPI * RB), 16, voff[u], 0, 0, 0);
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rv, (lds_void*)(vd + u * RPI * RB), 16, voff[u], 0, 0, 0);
+      }
     }
   }
 };
+
+// Tile loads land in LDS asynchronously: wait for this wave's, then the
+// barrier makes every wave's visible.
+__device__ inline void tile_loads_done() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
 
 // p0, p1 -> (hi, lo) bf16 pairs with p = hi + lo to about 2^-16 relative:
 // hi keeps the upper 16 bits of each value, lo is the exact fp32 remainder
@@ -216,25 +228,28 @@ __device__ inline LaneOffsets<D> lane_offsets(int lane) {
 // lane's row may see; MASKED is false when every key of the tile is visible
 // to every row of the workgroup.
 template <int D, bool MASKED>
-__device__ inline void compute_tile(const PrefillSmem<D>& sm, int b, int t0, int limit, int h,
-                                    const LaneOffsets<D>& lo, const bf16x8 (&qop)[D / 16], float scale_log2,
-                                    float& m_run, float& l_run, f32x16 (&acc)[D / 32]) {
+__device__ inline void compute_tile(const TileBuf<D>& tb, int t0, int limit, int h, const LaneOffsets<D>& lo,
+                                    const bf16x8 (&qop)[D / 16], float scale_log2, float& m_run, float& l_run,
+                                    f32x16 (&acc)[D / 32]) {
   constexpr int KS = D / 16;
   constexpr int NT = D / 32;
   constexpr int RB = D * 2;
-  const char* kt = sm.buf[b][0];
-  const char* vt = sm.buf[b][1];
+  const char* kt = tb.k;
+  const char* vt = tb.v;
 
-  f32x16 s[2] = {f32x16{}, f32x16{}};
+  // All K operands of the tile are read before the first product.
+  bf16x8 kop[KS][2];
 #pragma unroll
   for (int ks = 0; ks < KS; ++ks) {
     const int off = lo.k ^ (32 * ks);
 #pragma unroll
-    for (int sb = 0; sb < 2; ++sb) {
-      const bf16x8 a = *reinterpret_cast<const bf16x8*>(kt + off + 32 * sb * RB);
-      s[sb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qop[ks], s[sb], 0, 0, 0);
-    }
+    for (int sb = 0; sb < 2; ++sb) kop[ks][sb] = *reinterpret_cast<const bf16x8*>(kt + off + 32 * sb * RB);
   }
+  f32x16 s[2] = {f32x16{}, f32x16{}};
+#pragma unroll
+  for (int ks = 0; ks < KS; ++ks)
+#pragma unroll
+    for (int sb = 0; sb < 2; ++sb) s[sb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kop[ks][sb], qop[ks], s[sb], 0, 0, 0);
 
   // Raw scores keep their order (scale > 0), so the maximum is taken on them
   // and the scale enters once, in the exponent.
@@ -301,7 +316,7 @@ __global__ __launch_bounds__(kPrefillThreads, 2) void prefill_mfma_kernel(const 
   constexpr int KS = D / 16;
   constexpr int NT = D / 32;
   constexpr bool PAGED = LAYOUT != PLayout::kContig;
-  __shared__ PrefillSmem<D> sm;
+  __shared__ TileBuf<D> buf0, buf1;
   const int b = blockIdx.z, hk = blockIdx.y;
   const int qb = gridDim.x - 1 - blockIdx.x;
   const int TB = p.tokens_per_block;
@@ -329,8 +344,7 @@ __global__ __launch_bounds__(kPrefillThreads, 2) void prefill_mfma_kernel(const 
   const int qh = hk * p.group + g;
   const int limit = prefix + ic;
 
-  using Loader = TileLoader<D, LAYOUT>;
-  Loader ld;
+  TileLoader<D, LAYOUT> ld;
   ld.kbase = p.k + hk * p.stride_head + seq0 * p.stride_token;
   ld.vbase = p.v + hk * p.stride_head + seq0 * p.stride_token;
   ld.bt_row = PAGED ? p.block_table + static_cast<int64_t>(b) * p.max_pages : nullptr;
@@ -339,12 +353,10 @@ __global__ __launch_bounds__(kPrefillThreads, 2) void prefill_mfma_kernel(const 
   ld.page_shift = p.page_shift;
   ld.page_mask = p.page_mask;
   ld.kend = kend;
-  ld.c = threadIdx.x % Loader::CH;
-  ld.row0 = threadIdx.x / Loader::CH;
-  ld.voff = static_cast<uint32_t>(ld.row0 * p.stride_token + 16 * ld.c);
+  ld.init(uniform_i32(w), lane);
 
   ld.fetch_pages(0);
-  ld.load(0);
+  ld.load(buf0, 0);
   if (ntiles > 1) ld.fetch_pages(kPrefillTileKeys);
 
   // Q^T operand: row j, head_dim 16 ks + 8 h .. + 8.
@@ -360,29 +372,28 @@ __global__ __launch_bounds__(kPrefillThreads, 2) void prefill_mfma_kernel(const 
   for (int n = 0; n < NT; ++n) acc[n] = f32x16{};
   float m_run = -INFINITY, l_run = 0.f;
 
-  ld.store(sm, 0);
+  tile_loads_done();
   __syncthreads();
-  // Tiles every row sees whole, then the tiles that need the causal mask.
-  int t = 0;
-  for (; t < nfree; ++t) {
-    const bool more = t + 1 < ntiles;
-    if (more) {
-      ld.load(kPrefillTileKeys * (t + 1));
+  // Tile t is in buffer t % 2 while tile t + 1 streams into the other one.
+  // Tiles before nfree are visible to every row whole; later ones take the
+  // causal mask. The loop handles two tiles per pass so that each half names
+  // its buffers statically.
+  auto step = [&](const TileBuf<D>& cur, TileBuf<D>& nxt, int t) {
+    if (t + 1 < ntiles) {
+      ld.load(nxt, kPrefillTileKeys * (t + 1));
       if (t + 2 < ntiles) ld.fetch_pages(kPrefillTileKeys * (t + 2));
     }
-    compute_tile<D, false>(sm, t & 1, kPrefillTileKeys * t, limit, h, lo, qop, p.scale_log2, m_run, l_run, acc);
-    if (more) ld.store(sm, (t + 1) & 1);
-    __syncthreads();
-  }
-  for (; t < ntiles; ++t) {
-    const bool more = t + 1 < ntiles;
-    if (more) {
-      ld.load(kPrefillTileKeys * (t + 1));
-      if (t + 2 < ntiles) ld.fetch_pages(kPrefillTileKeys * (t + 2));
+    if (t < nfree) {
+      compute_tile<D, false>(cur, kPrefillTileKeys * t, limit, h, lo, qop, p.scale_log2, m_run, l_run, acc);
+    } else {
+      compute_tile<D, true>(cur, kPrefillTileKeys * t, limit, h, lo, qop, p.scale_log2, m_run, l_run, acc);
     }
-    compute_tile<D, true>(sm, t & 1, kPrefillTileKeys * t, limit, h, lo, qop, p.scale_log2, m_run, l_run, acc);
-    if (more) ld.store(sm, (t + 1) & 1);
+    tile_loads_done();
     __syncthreads();
+  };
+  for (int t = 0; t < ntiles; t += 2) {
+    step(buf0, buf1, t);
+    if (t + 1 < ntiles) step(buf1, buf0, t + 1);
   }
 
   l_run += __shfl_xor(l_run, 32);
