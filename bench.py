@@ -90,7 +90,11 @@ def _counter_medians(path):
 
 
 def _short_kernel_name(full):
-    """decode_mfma_queue_kernel<128, Layout 1> -> decode_mfma_queue_D128_paged (and similar)."""
+    """decode_mfma_queue_kernel<128, Layout 1, true> -> decode_mfma_queue_D128_paged_fp8 (and similar).
+
+    A bool template argument is the FP8 switch of the MFMA decode kernels
+    and the paged switch of the others.
+    """
     import re
 
     m = re.search(r"((?:decode|prefill)_\w+?)(?:_kernel)?<([^>]*)>", full)
@@ -109,6 +113,8 @@ def _short_kernel_name(full):
             name += "_bf16"
         elif a == "float":
             name += "_f32"
+        elif a in ("true", "false") and base.startswith("decode_mfma"):
+            name += "_fp8" if a == "true" else ""
         elif a in ("true", "false"):
             name += "_paged" if a == "true" else "_contig"
     return name
