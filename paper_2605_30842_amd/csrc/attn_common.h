@@ -65,7 +65,7 @@ template <int D>
 struct WaveState {
   float m[kWaves][kMaxGroup];   // running max (log2 units), -inf if no token seen
   float l[kWaves][kMaxGroup];   // sum of exp2(x - m)
-  float o[kWaves][kMaxGroup][D];  // sum of exp2(x - m) * v
+  alignas(16) float o[kWaves][kMaxGroup][D];  // sum of exp2(x - m) * v
 };
 
 __device__ inline int64_t uniform_i64(int64_t x) {

@@ -471,12 +471,16 @@ __device__ void attend_split(const AttnParams& p, SplitSmem<D, LAYOUT>& sm, int 
     sm.ws.m[w][c] = m_run;
     sm.ws.l[w][c] = l_run;
   }
+  // A lane's values of one head are NT consecutive head_dim positions, so
+  // they go out as 16-byte stores.
 #pragma unroll
   for (int r = 0; r < 4; ++r) {
     const int h = 4 * g + r;
     if (h < G) {
 #pragma unroll
-      for (int n = 0; n < NT; ++n) sm.ws.o[w][h][NT * c + n] = acc[n][r];
+      for (int n = 0; n < NT; n += 4)
+        *reinterpret_cast<float4*>(&sm.ws.o[w][h][NT * c + n]) =
+            make_float4(acc[n][r], acc[n + 1][r], acc[n + 2][r], acc[n + 3][r]);
     }
   }
   __syncthreads();
