@@ -89,6 +89,61 @@ def _counter_medians(path):
     return {k: sorted(v)[len(v) // 2] for k, v in vals.items()}
 
 
+# Counter passes of each workload (one rocprofv3 --pmc run each, within the
+# per-block limits: at most 8 SQ, 4 TCC and 2 GRBM counters per run).
+COUNTER_PASSES = {
+    "sq": "SQ_WAVES SQ_WAVE_CYCLES SQ_BUSY_CU_CYCLES SQ_ACTIVE_INST_VALU SQ_VALU_MFMA_BUSY_CYCLES SQ_INSTS_LDS "
+          "SQ_LDS_IDX_ACTIVE SQ_LDS_BANK_CONFLICT GRBM_GUI_ACTIVE GRBM_COUNT",
+    "tcc": "TCC_HIT_sum TCC_MISS_sum TCC_EA0_RDREQ_sum TCC_BUBBLE_sum",
+    "tcc2": "TCC_EA0_RDREQ_32B_sum TCC_EA0_RDREQ_DRAM_sum",
+}
+
+
+def _gpu_agent(path):
+    for f in glob.glob(os.path.join(path, "**", "*agent_info.csv"), recursive=True):
+        for r in csv.DictReader(open(f)):
+            if r.get("Agent_Type") == "GPU":
+                return r
+    return None
+
+
+def _derived_counters(d, tag, kv_bytes):
+    """Occupancy, VALU / MFMA busy, LDS bank conflicts, L2 hits and EA read bytes of the attention kernel.
+
+    Medians over its dispatches of the passes in COUNTER_PASSES; None if the
+    runs are absent. The busy and conflict percentages use rocprofv3's own
+    definitions (VALUBusy, MfmaUtil, LDSBankConflict) with the GPU-active
+    cycles of one XCD (a dispatch row sums GRBM_GUI_ACTIVE over the XCDs).
+    SQ_WAVE_CYCLES / SQ_BUSY_CU_CYCLES (both in quad-cycles, summed over
+    SIMDs) is the mean number of resident waves per SIMD while busy: it reads
+    1.0 for a grid of one 4-wave workgroup per CU. Read bytes come from
+    FETCH_SIZE with the copy calibration, not from the request counts, whose
+    size classes (TCC_BUBBLE reads 0) do not add up on this GPU.
+    """
+    m = {}
+    for sub in COUNTER_PASSES:
+        for (kind, name), v in _counter_medians(os.path.join(d, "pmc", f"{tag}_{sub}")).items():
+            if kind == "attn":
+                m[name] = v
+    ag = _gpu_agent(os.path.join(d, "pmc", f"{tag}_sq"))
+    if "SQ_WAVES" not in m or "TCC_HIT_sum" not in m or ag is None:
+        return None
+    cu, simd, xcc = int(ag["Cu_Count"]), int(ag["Simd_Count"]), int(ag["Num_Xcc"])
+    gui = m["GRBM_GUI_ACTIVE"] / xcc
+    out = {"raw": {k: m[k] for k in sorted(m)},
+           "waves": int(m["SQ_WAVES"]),
+           "mean_waves_per_simd_while_busy": round(m["SQ_WAVE_CYCLES"] / m["SQ_BUSY_CU_CYCLES"], 2),
+           "simds_per_cu": int(ag["Simd_Per_Cu"]),
+           "valu_busy_pct": round(100 * m["SQ_ACTIVE_INST_VALU"] / cu / gui, 2),
+           "mfma_util_pct": round(100 * m["SQ_VALU_MFMA_BUSY_CYCLES"] / (gui * simd), 2),
+           "lds_bank_conflict_pct": round(100 * m["SQ_LDS_BANK_CONFLICT"] / gui / cu, 3),
+           "lds_conflict_cycles_per_active_cycle": round(m["SQ_LDS_BANK_CONFLICT"] / max(m["SQ_LDS_IDX_ACTIVE"], 1), 4),
+           "l2_hit_pct": round(100 * m["TCC_HIT_sum"] / max(m["TCC_HIT_sum"] + m["TCC_MISS_sum"], 1), 2)}
+    if "TCC_EA0_RDREQ_DRAM_sum" in m:
+        out["ea_read_requests_to_dram_pct"] = round(100 * m["TCC_EA0_RDREQ_DRAM_sum"] / max(m["TCC_EA0_RDREQ_sum"], 1), 2)
+    return out
+
+
 def _short_kernel_name(full):
     """decode_mfma_queue_kernel<128, Layout 1, true> -> decode_mfma_queue_D128_paged_fp8 (and similar).
 
@@ -182,6 +237,7 @@ def summarize(a):
         rec.update({"fetch_KiB_per_dispatch": fm, "write_KiB_per_dispatch": wm, "fetch_scale": fetch_scale,
                     "write_scale": write_scale, "traffic_bytes": traffic,
                     "traffic_over_kv_bytes": round(traffic / kv, 4) if traffic else None})
+        counters = _derived_counters(d, f"{tag}{i}", kv)
         name = f"{kname}_{spec.name}.md"
         with open(os.path.join(PROFILES, name), "w") as f:
             f.write(f"# {kname} on {spec.name}\n\n")
@@ -195,6 +251,10 @@ def summarize(a):
                         f"python3 bench.py {pmc_args}\n")
                 f.write(f"rocprofv3 --pmc {c} --output-format csv -d {d}/pmc/copy_{sub} -o copy_{sub} -- "
                         f"python3 bench.py --probe copy --probe-bytes {COPY_CAL_BYTES} --steps 3 --warmup 1\n")
+            if counters:
+                for sub, names in COUNTER_PASSES.items():
+                    f.write(f"rocprofv3 --pmc {names} --output-format csv -d {d}/pmc/{tag}{i}_{sub} -o {tag}{i}_{sub}"
+                            f" -- python3 bench.py {pmc_args}\n")
             f.write(f"python3 bench.py --summarize {d}\n```\n\n")
             f.write("Kernel statistics (rocprofv3 --stats, all dispatches of the bench run):\n\n")
             f.write("| kernel | calls | avg us | min us | max us |\n|---|---|---|---|---|\n")
@@ -204,6 +264,15 @@ def summarize(a):
             f.write("\nHBM traffic per dispatch: FETCH_SIZE and WRITE_SIZE medians (KiB), each scaled by the factor "
                     f"that makes the same counter read {COPY_CAL_BYTES} bytes for a copy of that size.\n\n")
             f.write("```json\n" + json.dumps(rec, indent=1) + "\n```\n")
+            if counters:
+                f.write("\nCounters (medians over the kernel's dispatches in the --pmc runs above; percentages as "
+                        "rocprofv3 defines VALUBusy, MfmaUtil and LDSBankConflict, over one XCD's GPU-active cycles; "
+                        "rocprofv3 exposes no Infinity Cache (MALL) counters on this system):\n\n")
+                f.write("| quantity | value |\n|---|---|\n")
+                for k, v in counters.items():
+                    if k != "raw":
+                        f.write(f"| {k} | {v} |\n")
+                f.write("\n```json\n" + json.dumps({"counters_raw": counters["raw"]}, indent=1) + "\n```\n")
         print(f"wrote profiles/{name}", flush=True)
 
 

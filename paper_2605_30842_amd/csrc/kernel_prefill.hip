@@ -311,14 +311,37 @@ __device__ inline void compute_tile(const TileBuf<D>& tb, int t0, int limit, int
 // Grid: (query blocks, KV heads, sequences). Query blocks are taken in
 // reverse order so that, for causal attention, the blocks with the most keys
 // start first.
+constexpr int kXcds = 8;  // XCDs of the GPU; workgroups are dealt to them round robin
+
 template <int D, PLayout LAYOUT>
 __global__ __launch_bounds__(kPrefillThreads, 2) void prefill_mfma_kernel(const PrefillParams p) {
   constexpr int KS = D / 16;
   constexpr int NT = D / 32;
   constexpr bool PAGED = LAYOUT != PLayout::kContig;
   __shared__ TileBuf<D> buf0, buf1;
-  const int b = blockIdx.z, hk = blockIdx.y;
-  const int qb = gridDim.x - 1 - blockIdx.x;
+  // Work item of the workgroup. Workgroups go to the XCDs in turn (linear
+  // id modulo 8). When the (sequence, KV head) pairs divide evenly over the
+  // XCDs, pair hb runs all its query blocks on XCD hb % 8, so the K/V tiles
+  // those blocks all stream are shared in that XCD's L2. An XCD runs its
+  // pairs one after the other, so that its resident workgroups work on few
+  // pairs at a time, and the blocks of a pair in order of q, the block's place
+  // counted from the sequence's last (heaviest) block. Otherwise the grid
+  // order is kept, with q = blockIdx.x.
+  int b, hk, q;
+  const int pairs = gridDim.y * gridDim.z;
+  if (pairs % kXcds == 0) {
+    const int lin = blockIdx.x + gridDim.x * (blockIdx.y + gridDim.y * blockIdx.z);
+    const int x = lin % kXcds, k = lin / kXcds;
+    const int r = k / gridDim.x;
+    q = k - r * static_cast<int>(gridDim.x);
+    const int hb = x + kXcds * r;
+    b = hb / gridDim.y;
+    hk = hb - b * static_cast<int>(gridDim.y);
+  } else {
+    b = blockIdx.z;
+    hk = blockIdx.y;
+    q = blockIdx.x;
+  }
   const int TB = p.tokens_per_block;
 
   int L = p.ctx_lens[b];
@@ -327,8 +350,10 @@ __global__ __launch_bounds__(kPrefillThreads, 2) void prefill_mfma_kernel(const 
   int64_t seq0 = PAGED ? 0 : p.seq_start[b];
   asm volatile("" : "+s"(L), "+s"(M), "+s"(qs), "+s"(seq0));  // one round trip for all four
   M = min(M, L);
-  const int i0 = qb * TB;
-  if (i0 >= M) return;
+  // q counts from each sequence's last (heaviest) block of new tokens.
+  const int nblk = (M + TB - 1) / TB;
+  if (q >= nblk) return;
+  const int i0 = (nblk - 1 - q) * TB;
   const int prefix = L - M;
   const int kend = prefix + min(M, i0 + TB);  // keys any row of this block sees
   const int ntiles = (kend + kPrefillTileKeys - 1) / kPrefillTileKeys;
