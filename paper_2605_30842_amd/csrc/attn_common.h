@@ -224,60 +224,74 @@ __device__ void finalize_split(const AttnParams& p, const WaveState<D>& ws, int 
   }
   __syncthreads();
   if (!sm_last) return;
-  if (tid == 0) atomicExch(&p.tickets[b * p.num_kv_heads + hk], 0u);
 
-  // Merge over splits in one pass. When there are fewer slots than threads,
-  // tps threads share a slot, taking splits sub, sub + tps, ...; their states
-  // are then merged in sub order. Each split part has weight sum 1 (it is
-  // normalised) and log-weight lse2.
+  // Merge over splits. With fewer slots than threads, tps adjacent lanes
+  // share a slot and take splits sub, sub + tps, ... Each lane visits its
+  // splits in batches of kMergeBatch whose loads are all in flight together;
+  // a batch's largest log-weight is found first, so its part weights are
+  // independent exponentials and its sums plain multiply-add chains, and the
+  // batch folds into the lane's running state with one rescale. The lanes of
+  // a slot then combine their states by lane shuffles. Every sum has a fixed
+  // order, so results do not depend on timing. Each split part has weight
+  // sum 1 (it is normalised) and log-weight lse2.
   const int tps = slots >= kThreads ? 1 : kThreads / slots;
-  __shared__ float4 sm_acc[kThreads];
-  __shared__ float sm_m[kThreads];
-  __shared__ float sm_w[kThreads];
   for (int slot = tid / tps; slot < slots; slot += kThreads / tps) {
     const int sub = tid % tps;
     const int h = (slot * 4) / D;
     const int d0 = slot * 4 - h * D;
-    MergeState st;
-    // Batches of kMergeBatch splits: all loads of a batch are in flight
-    // together. Indices past the last split re-read the last one and get
-    // weight 0.
+    float m = -INFINITY, wsum = 0.f;
+    float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
     for (int s0 = sub; s0 < nsplit_b; s0 += kMergeBatch * tps) {
       float l2[kMergeBatch];
       float4 o[kMergeBatch];
 #pragma unroll
       for (int i = 0; i < kMergeBatch; ++i) {
-        const int si = min(s0 + i * tps, nsplit_b - 1);
+        const int si = min(s0 + i * tps, nsplit_b - 1);  // past the last split: re-read it, weight 0
         l2[i] = load_coherent(rl, (si * G + h) * 4);
         o[i] = load4_coherent(ro, ((si * G + h) * D + d0) * 4);
       }
+      float mb = -INFINITY;
 #pragma unroll
-      for (int i = 0; i < kMergeBatch; ++i) st.add(s0 + i * tps < nsplit_b ? l2[i] : -INFINITY, 1.f, o[i]);
+      for (int i = 0; i < kMergeBatch; ++i) {
+        if (s0 + i * tps >= nsplit_b) l2[i] = -INFINITY;
+        mb = fmaxf(mb, l2[i]);
+      }
+      const float mn = fmaxf(m, mb);
+      const float ref = mn == -INFINITY ? 0.f : mn;
+      const float a = fast_exp2(m - ref);
+      acc = make_float4(acc.x * a, acc.y * a, acc.z * a, acc.w * a);
+      wsum *= a;
+#pragma unroll
+      for (int i = 0; i < kMergeBatch; ++i) {
+        const float w = fast_exp2(l2[i] - ref);
+        wsum += w;
+        acc = make_float4(fmaf(w, o[i].x, acc.x), fmaf(w, o[i].y, acc.y), fmaf(w, o[i].z, acc.z),
+                          fmaf(w, o[i].w, acc.w));
+      }
+      m = mn;
     }
-    if (tps == 1) {
-      const float inv = p.out_scale / st.wsum;
+    for (int off = 1; off < tps; off <<= 1) {
+      MergeState st;
+      st.m = m;
+      st.wsum = wsum;
+      st.acc = acc;
+      st.add(__shfl_xor(m, off), __shfl_xor(wsum, off),
+             make_float4(__shfl_xor(acc.x, off), __shfl_xor(acc.y, off), __shfl_xor(acc.z, off),
+                         __shfl_xor(acc.w, off)));
+      m = st.m;
+      wsum = st.wsum;
+      acc = st.acc;
+    }
+    if (sub == 0) {
+      const float inv = p.out_scale / wsum;
       *reinterpret_cast<float4*>(p.out + static_cast<int64_t>(head0 + h) * D + d0) =
-          make_float4(st.acc.x * inv, st.acc.y * inv, st.acc.z * inv, st.acc.w * inv);
-      if (d0 == 0 && p.lse != nullptr) p.lse[head0 + h] = (st.m + log2f(st.wsum)) * kLn2;
-    } else {
-      sm_acc[tid] = st.acc;
-      sm_m[tid] = st.m;
-      sm_w[tid] = st.wsum;
+          make_float4(acc.x * inv, acc.y * inv, acc.z * inv, acc.w * inv);
+      if (d0 == 0 && p.lse != nullptr) p.lse[head0 + h] = (m + log2f(wsum)) * kLn2;
     }
   }
-  if (tps == 1) return;
-  __syncthreads();
-  if (tid % tps == 0) {
-    const int slot = tid / tps;
-    const int h = (slot * 4) / D;
-    const int d0 = slot * 4 - h * D;
-    MergeState st;
-    for (int i = 0; i < tps; ++i) st.add(sm_m[tid + i], sm_w[tid + i], sm_acc[tid + i]);
-    const float inv = p.out_scale / st.wsum;
-    *reinterpret_cast<float4*>(p.out + static_cast<int64_t>(head0 + h) * D + d0) =
-        make_float4(st.acc.x * inv, st.acc.y * inv, st.acc.z * inv, st.acc.w * inv);
-    if (d0 == 0 && p.lse != nullptr) p.lse[head0 + h] = (st.m + log2f(st.wsum)) * kLn2;
-  }
+  // Back to zero for the next call. Issued after the merge's loads, which
+  // would otherwise wait for it (memory operations complete in order).
+  if (tid == 0) atomicExch(&p.tickets[b * p.num_kv_heads + hk], 0u);
 }
 
 }  // namespace comem
