@@ -70,10 +70,17 @@ def _args():
 
 
 def kernel_source_hash(sources=KERNEL_SOURCES) -> str:
+    """Hash of the sources' code: comments and whitespace do not count, so a
+    recorded profile stays valid across edits that change no code."""
+    import re
+
     h = hashlib.sha256()
     for rel in sources:
-        with open(os.path.join(ROOT, rel), "rb") as f:
-            h.update(f.read())
+        with open(os.path.join(ROOT, rel), encoding="utf-8") as f:
+            text = f.read()
+        text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)
+        text = re.sub(r"//[^\n]*", " ", text)
+        h.update(" ".join(text.split()).encode())
     return h.hexdigest()[:16]
 
 

@@ -308,9 +308,8 @@ __device__ inline void compute_tile(const TileBuf<D>& tb, int t0, int limit, int
   l_run += psum;
 }
 
-// Grid: (query blocks, KV heads, sequences). Query blocks are taken in
-// reverse order so that, for causal attention, the blocks with the most keys
-// start first.
+// Grid: (query blocks, KV heads, sequences); the kernel maps the workgroup
+// id to a work item itself (see the top of the kernel).
 constexpr int kXcds = 8;  // XCDs of the GPU; workgroups are dealt to them round robin
 
 template <int D, PLayout LAYOUT>
