@@ -29,7 +29,7 @@ constexpr uint64_t kPlanMagic = 0x434f4d454d444131ull;  // "COMEMDA1"
 constexpr int kAssumedCUs = 256;                        // gfx950 (MI355X) without a device query
 constexpr int64_t kTargetWgsPerCu = 2;                  // workgroups per compute unit for one full round
 constexpr int kQueueWgsPerCu = 2;                       // resident workgroups per compute unit (MFMA kernel)
-constexpr int64_t kMinChunk = 256;                      // tokens per split, lower bound
+constexpr int64_t kMinChunk = 64;                       // tokens per split, lower bound
 constexpr int64_t kMaxChunk = 2048;                     // tokens per split, upper bound (auto plan)
 constexpr int64_t kMaxContext = int64_t{1} << 30;
 constexpr int kGridYZLimit = 65535;
