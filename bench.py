@@ -469,6 +469,9 @@ def main():
         print(f"bench.py runs on one GPU only (asked for --gpus {a.gpus}); this build has no multi-GPU path.",
               file=sys.stderr)
         sys.exit(2)
+    if a.steps < 1 or a.warmup < 0:
+        print("--steps must be at least 1 and --warmup at least 0", file=sys.stderr)
+        sys.exit(2)
     if a.probe:
         _probe(a)
         return
@@ -558,23 +561,29 @@ def main():
     if a.timing == "graph":
         # One graph holds at least 16 launches, cycling over the KV copies, so
         # the gap between graph launches is spread over many steps; the timed
-        # region replays it.
+        # region replays it, and a second graph of the remaining launches
+        # (the copies continue in order), so that exactly `steps` are timed.
         per_graph = copies * max(1, -(-16 // copies))
-        graph = torch.cuda.CUDAGraph()
-        side = torch.cuda.Stream()
-        side.wait_stream(stream)
-        with torch.cuda.graph(graph, stream=side):
-            for i in range(per_graph):
-                step(i, torch.cuda.current_stream())
-        torch.cuda.synchronize()
-        for _ in range(3):  # every replay must reproduce the eager result bit for bit
-            out.zero_()
-            graph.replay()
+        full, rem = divmod(a.steps, per_graph)
+
+        def capture(n):
+            g = torch.cuda.CUDAGraph()
+            side = torch.cuda.Stream()
+            side.wait_stream(stream)
+            with torch.cuda.graph(g, stream=side):
+                for i in range(n):
+                    step(i, torch.cuda.current_stream())
             torch.cuda.synchronize()
-            assert torch.equal(out, eager_out), "graph replay differs from eager result"
-        replays = max(1, -(-a.steps // per_graph))
-        steps = replays * per_graph
-        ms = timed(lambda: [graph.replay() for _ in range(replays)], steps)
+            return g
+
+        graphs = [capture(per_graph)] * full + ([capture(rem)] if rem else [])
+        for g in set(graphs):
+            for _ in range(3):  # every replay must reproduce the eager result bit for bit (the copies are equal)
+                out.zero_()
+                g.replay()
+                torch.cuda.synchronize()
+                assert torch.equal(out, eager_out), "graph replay differs from eager result"
+        ms = timed(lambda: [g.replay() for g in graphs], a.steps)
     if a.op == "append":
         row_bytes = spec.batch * spec.num_kv_heads * spec.head_dim * spec.elem_bytes * 2  # K and V rows
         moved = 2 * row_bytes  # each row read once and written once
