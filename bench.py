@@ -69,6 +69,17 @@ def _args():
     return ap.parse_args()
 
 
+def _cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
 def kernel_source_hash(sources=KERNEL_SOURCES) -> str:
     """Hash of the sources' code: comments and whitespace do not count, so a
     recorded profile stays valid across edits that change no code."""
@@ -359,7 +370,7 @@ def _cpu_baseline(w, budget_s):
               f"query heads) of the same workload, float64 numpy")
     return {"value": round(per_bytes / dt / 1e9, 3), "unit": "GB/s", "cores": threads, "kind": "oracle",
             "sample": sample, "seconds_per_call": round(dt, 4),
-            "host_cpus": len(os.sched_getaffinity(0))}
+            "host_cpus": len(os.sched_getaffinity(0)), "cpu_model": _cpu_model()}
 
 
 def _prefill_cpu_baseline(pw, budget_s):
@@ -389,7 +400,7 @@ def _prefill_cpu_baseline(pw, budget_s):
     return {"value": round(flops / dt / 1e12, 6), "unit": "TFLOP/s", "cores": threads, "kind": "oracle",
             "sample": f"{reps} oracle calls over the last {min(M, 8)} new tokens x {s.num_q_heads} heads of "
                       f"sequence 0 ({L} cached tokens), float64 numpy",
-            "seconds_per_call": round(dt, 4), "host_cpus": len(os.sched_getaffinity(0))}
+            "seconds_per_call": round(dt, 4), "host_cpus": len(os.sched_getaffinity(0)), "cpu_model": _cpu_model()}
 
 
 def _prefill(a):
@@ -602,6 +613,16 @@ def main():
         return
     gbps = kv_bytes / (ms * 1e-3) / 1e9
     assert torch.isfinite(out).all().item()
+    # Spread of single calls (after the timed region): each of 100 eager
+    # calls bracketed by its own pair of events on the stream.
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(100)]
+    for i, (b0, b1) in enumerate(ev):
+        b0.record(stream)
+        step(i, stream)
+        b1.record(stream)
+    torch.cuda.synchronize()
+    per_call = sorted(b0.elapsed_time(b1) * 1e3 for b0, b1 in ev)
+    pct = {f"p{q}": round(per_call[min(len(per_call) - 1, q * len(per_call) // 100)], 3) for q in (10, 50, 90)}
 
     cpu = _cpu_baseline(w, a.cpu_seconds) if a.cpu_seconds > 0 and a.op == "attention" else None
     kind = a.variant if a.variant != "auto" else ("valu" if spec.dtype == "f32" else "mfma")
@@ -627,6 +648,7 @@ def main():
             "layout": spec.layout, "page_size": spec.page_size, "kv_bytes_per_step": kv_bytes,
             "kv_copies_cycled": copies, "chunk_tokens": chunk, "splits": splits, "kernel": kind,
             "timing": a.timing, "eager_us_per_step": round(eager_ms * 1e3, 3), "op": a.op,
+            "single_call_us": pct,
         },
         "roofline": {
             "bound": "hbm", "achieved": round(gbps, 2), "peak": PEAK_HBM_GBPS, "unit": "GB/s",
