@@ -118,7 +118,11 @@ comem_status comem_decode_attn_destroy(comem_decode_attn_plan* plan);
 const char* comem_status_string(comem_status status);
 
 /* Tokens per split and number of splits a call would use (for tests and
- * reports): same planning as the compute calls. */
+ * reports): same planning as the contiguous compute call. A paged call with
+ * pages of 1 or 2 tokens may plan shorter splits, so that the block-table
+ * entries of one split fit the matrix-core kernel's on-chip copy (2048
+ * entries); a configured chunk_tokens that does not fit is refused with
+ * COMEM_ERR_INVALID_SHAPE. */
 comem_status comem_decode_attn_plan_splits(const comem_decode_attn_plan* plan, int32_t batch,
                                            int64_t max_ctx_len, size_t workspace_bytes,
                                            int32_t* chunk_tokens_out, int32_t* num_splits_out);

@@ -2,6 +2,7 @@
 // any HIP call), split planning, kernel selection and launch.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cmath>
 #include <cstdint>
 #include <cstring>
@@ -85,17 +86,26 @@ int64_t mfma_chunk(const comem_decode_attn_plan& p, int64_t batch, int64_t L) {
   return 1024;
 }
 
-// Choose tokens per split and the split count for one call.
-comem_status plan_call(const comem_decode_attn_plan& p, int64_t batch, int64_t max_ctx,
+// Largest split, in tokens, whose block-table entries fit the matrix-core
+// kernel's LDS copy (a multiple of 32), for pages of `page_size` tokens.
+int64_t mfma_page_cap(int64_t page_size) {
+  return std::max<int64_t>(32, (comem::mfma_max_split_pages() - 2) * page_size / 32 * 32);
+}
+
+// Choose tokens per split and the split count for one call. page_size is 0
+// for a contiguous cache; for a paged one the matrix-core kernel's planned
+// splits stay within the pages its LDS copy of the block table holds.
+comem_status plan_call(const comem_decode_attn_plan& p, int64_t batch, int64_t max_ctx, int64_t page_size,
                        size_t ws_bytes, int64_t* chunk_out, int64_t* splits_out) {
   const int64_t L = max_ctx > 0 ? max_ctx : 1;
+  const int64_t cap = page_size > 0 && uses_mfma(p) ? mfma_page_cap(page_size) : INT64_MAX;
   int64_t chunk;
   if (p.cfg.chunk_tokens > 0) {
     chunk = p.cfg.chunk_tokens;
     if (call_workspace_bytes(p, batch, ceil_div(L, chunk)) > ws_bytes) return COMEM_ERR_WORKSPACE_TOO_SMALL;
   } else {
     if (uses_mfma(p)) {
-      chunk = mfma_chunk(p, batch, L);
+      chunk = std::min(mfma_chunk(p, batch, L), cap);
     } else {
       const int64_t target = kTargetWgsPerCu * p.num_cus;
       const int64_t per = ceil_div(batch * p.cfg.num_kv_heads * L, target);
@@ -103,7 +113,7 @@ comem_status plan_call(const comem_decode_attn_plan& p, int64_t batch, int64_t m
       while (chunk < per && chunk < kMaxChunk) chunk *= 2;
     }
     while (call_workspace_bytes(p, batch, ceil_div(L, chunk)) > ws_bytes) {
-      if (chunk >= L) return COMEM_ERR_WORKSPACE_TOO_SMALL;
+      if (chunk >= L || chunk * 2 > cap) return COMEM_ERR_WORKSPACE_TOO_SMALL;
       chunk *= 2;
     }
   }
@@ -314,7 +324,7 @@ comem_status decode_contiguous(const comem_decode_attn_plan* plan, const void* q
     if (!aligned(new_k, 16) || !aligned(new_v, 16)) return COMEM_ERR_MISALIGNED;
   }
   int64_t chunk = 0, splits = 0;
-  st = plan_call(*p, batch, max_ctx_len, workspace == nullptr ? 0 : workspace_bytes, &chunk, &splits);
+  st = plan_call(*p, batch, max_ctx_len, 0, workspace == nullptr ? 0 : workspace_bytes, &chunk, &splits);
   if (st != COMEM_OK) return st;
   if (p->device == COMEM_NO_DEVICE) return COMEM_ERR_NO_DEVICE;
   const bool queue = uses_queue(*p, batch, workspace, workspace_bytes);
@@ -347,9 +357,10 @@ comem_status decode_paged(const comem_decode_attn_plan* plan, const void* q, con
     if (!aligned(new_k, 16) || !aligned(new_v, 16)) return COMEM_ERR_MISALIGNED;
   }
   int64_t chunk = 0, splits = 0;
-  st = plan_call(*p, batch, max_ctx_len, workspace == nullptr ? 0 : workspace_bytes, &chunk, &splits);
+  st = plan_call(*p, batch, max_ctx_len, page_size, workspace == nullptr ? 0 : workspace_bytes, &chunk, &splits);
   if (st != COMEM_OK) return st;
-  // The matrix-core kernel stages one split's block-table entries in LDS.
+  // The matrix-core kernel stages one split's block-table entries in LDS (a
+  // planned split always fits; a configured chunk_tokens may not).
   if (uses_mfma(*p) && (chunk - 1) / page_size + 2 > comem::mfma_max_split_pages()) return COMEM_ERR_INVALID_SHAPE;
   if (p->device == COMEM_NO_DEVICE) return COMEM_ERR_NO_DEVICE;
   const bool queue = uses_queue(*p, batch, workspace, workspace_bytes);
@@ -500,7 +511,7 @@ comem_status comem_decode_attn_plan_splits(const comem_decode_attn_plan* plan, i
   if (batch < 0 || batch > p->cfg.max_batch) return COMEM_ERR_INVALID_SHAPE;
   if (max_ctx_len < 0 || max_ctx_len > p->cfg.max_ctx_len) return COMEM_ERR_INVALID_SHAPE;
   int64_t chunk = 0, splits = 0;
-  const comem_status st = plan_call(*p, batch, max_ctx_len, workspace_bytes, &chunk, &splits);
+  const comem_status st = plan_call(*p, batch, max_ctx_len, 0, workspace_bytes, &chunk, &splits);
   if (st != COMEM_OK) return st;
   *chunk_tokens_out = static_cast<int32_t>(chunk);
   *num_splits_out = static_cast<int32_t>(splits);

@@ -192,6 +192,34 @@ def test_paged_validation(plan, kw, status):
     assert B.load_library().comem_decode_attn_paged(*_paged_args(p, ws, **kw).values()) == status
 
 
+@pytest.mark.parametrize("page_size", [1, 2, 16])
+def test_planned_splits_fit_the_page_table_copy(page_size):
+    """A planned split of a long paged context never needs more block-table
+    entries than the matrix-core kernel copies to LDS: with 1- and 2-token
+    pages the planner shortens its 4096-token splits instead of refusing the
+    call (the call then stops only for want of a device)."""
+    L = 262144
+    p, ws = B.comem_decode_attn_init(_cfg(max_batch=1, max_ctx_len=L), B.NO_DEVICE)
+    try:
+        args = _paged_args(p, ws, page_size=page_size, num_pages=L, max_pages=L // page_size, batch=1,
+                           max_ctx_len=L, stride_page=page_size * 8 * 128)
+        assert B.load_library().comem_decode_attn_paged(*args.values()) == B.ERR_NO_DEVICE
+    finally:
+        B.comem_decode_attn_destroy(p)
+
+
+def test_configured_split_too_long_for_the_page_table_copy():
+    """A chunk_tokens the caller fixed is not shortened: 4096 one-token pages per split are refused."""
+    L = 262144
+    p, ws = B.comem_decode_attn_init(_cfg(max_batch=1, max_ctx_len=L, chunk_tokens=4096), B.NO_DEVICE)
+    try:
+        args = _paged_args(p, ws, page_size=1, num_pages=L, max_pages=L, batch=1, max_ctx_len=L,
+                           stride_page=8 * 128)
+        assert B.load_library().comem_decode_attn_paged(*args.values()) == B.ERR_INVALID_SHAPE
+    finally:
+        B.comem_decode_attn_destroy(p)
+
+
 def _append_args(plan, **kw):
     args = dict(plan=plan, new_k=A, new_v=A, k=A, v=A, stride_token=8 * 128, stride_head=128, seq_start=A,
                 ctx_lens=A, batch=2, max_ctx_len=4096, stream=None)

@@ -85,6 +85,16 @@ def test_paged_small(variant, ps):
     check(out, lse, ro, rl, "bf16", f"paged ps={ps} {variant}")
 
 
+@pytest.mark.parametrize("ps", [1, 2])
+def test_long_context_tiny_pages_planned(ps):
+    """140000 tokens in 1- or 2-token pages: the planner shortens its 4096-token
+    splits (to 2016 / 4064) so that a split's block-table entries fit the
+    kernel's LDS copy; the result still matches the oracle."""
+    spec = small_spec(WORKLOADS[4], [140000], seed=60 + ps).replace(page_size=ps)
+    _, _, _, out, lse, ro, rl = _case(spec)
+    check(out, lse, ro, rl, "bf16", f"long context, page size {ps}")
+
+
 @pytest.mark.parametrize("variant", ["mfma", "mfma_grid", "valu"])
 def test_empty_and_one_token(variant):
     spec = small_spec(WORKLOADS[2], [0, 1, 0, 1, 2], seed=26)
