@@ -34,10 +34,18 @@
  * Errors: every argument is checked on the host before any HIP call; a bad
  * argument returns its status and enqueues nothing. Launch failures return
  * COMEM_ERR_HIP. The library never aborts, exits or throws across this ABI.
- * Device-side contract (not checked): 0 <= ctx_lens[b] <= max_ctx_len,
- * contexts lie inside the given buffers, and for the paged call
- * 0 <= block_table[b][i] < num_pages for every i < ceil(ctx_lens[b] /
- * page_size). Block-table entries past that are never read.
+ * Device-side contract: 0 <= ctx_lens[b] <= max_ctx_len, contexts lie
+ * inside the given buffers, and for the paged call 0 <= block_table[b][i] <
+ * num_pages for every i < ceil(ctx_lens[b] / page_size). Block-table entries
+ * past that are never read. The kernels hold the first and the last part of
+ * the contract themselves: a length outside [0, max_ctx_len] is clamped into
+ * it, and an entry outside [0, num_pages) is read as page 0 and never written
+ * through (the fused append skips the store). A violation therefore gives
+ * wrong results for its sequence but no access outside the page pool or the
+ * workspace. With COMEM_FLAG_DEBUG_CHECKS in the plan's flags, every violation
+ * also sets its COMEM_DEVICE_ERR_* bit in an error word in the workspace,
+ * which comem_decode_attn_device_errors reads. Whether a contiguous context
+ * lies inside its buffer cannot be checked (the buffer sizes are not passed).
  */
 #ifndef COMEM_DECODE_ATTN_H
 #define COMEM_DECODE_ATTN_H
@@ -78,6 +86,13 @@ typedef enum {
   COMEM_VARIANT_MFMA_GRID = 3 /* matrix-core kernel, always one workgroup per split */
 } comem_variant;
 
+/* Plan flags (comem_decode_attn_config.flags). */
+#define COMEM_FLAG_DEBUG_CHECKS 1u /* record device-side contract violations (needs a workspace) */
+
+/* Bits of the device error word (COMEM_FLAG_DEBUG_CHECKS). */
+#define COMEM_DEVICE_ERR_CTX_LEN 1u     /* some ctx_lens[b] outside [0, max_ctx_len] (clamped) */
+#define COMEM_DEVICE_ERR_BLOCK_TABLE 2u /* some block-table entry read outside [0, num_pages) */
+
 /* Pass as `device` to comem_decode_attn_init to make a plan without touching
  * the HIP runtime (a gfx950 with 256 compute units is assumed). Such a plan
  * sizes workspaces and validates arguments; compute calls with it return
@@ -96,6 +111,7 @@ typedef struct {
   int32_t variant;      /* comem_variant (fp8 caches: not COMEM_VARIANT_VALU) */
   float k_scale;        /* COMEM_FP8_E4M3 only: finite and > 0, the per-tensor K scale */
   float v_scale;        /* COMEM_FP8_E4M3 only: finite and > 0, the per-tensor V scale */
+  uint32_t flags;       /* 0 or COMEM_FLAG_DEBUG_CHECKS */
 } comem_decode_attn_config;
 
 typedef struct comem_decode_attn_plan comem_decode_attn_plan;
@@ -126,6 +142,17 @@ const char* comem_status_string(comem_status status);
 comem_status comem_decode_attn_plan_splits(const comem_decode_attn_plan* plan, int32_t batch,
                                            int64_t max_ctx_len, size_t workspace_bytes,
                                            int32_t* chunk_tokens_out, int32_t* num_splits_out);
+
+/* Device-side contract violations (plan made with COMEM_FLAG_DEBUG_CHECKS):
+ * waits for hip_stream, stores in *errors_out the COMEM_DEVICE_ERR_* bits
+ * that calls using this workspace have set since the last read, and clears
+ * them. It synchronises the stream and copies four bytes to the host, so it
+ * is for tests and debugging, not for the decode loop, and must not be
+ * captured in a graph. workspace and workspace_bytes are those of the calls.
+ * The standalone append calls take no workspace and record nothing; their
+ * kernel skips a sequence that violates the contract. */
+comem_status comem_decode_attn_device_errors(const comem_decode_attn_plan* plan, void* workspace,
+                                             size_t workspace_bytes, uint32_t* errors_out, void* hip_stream);
 
 /* Contiguous / ragged cache (paper Sec. 2.2: K_cache, V_cache of l tokens,
  * each token an [h_kv, d_h] block). Strides count elements of the cache's

@@ -30,12 +30,16 @@
  *
  * Ownership: the caller owns every device buffer. Errors: as for the decode
  * calls, every argument is checked on the host before any HIP call and a bad
- * argument returns its status with nothing enqueued. Device-side contract
- * (not checked): 0 <= q_lens[b] <= ctx_lens[b] <= max_ctx_len, q_lens[b] <=
- * max_q_len, contexts and query rows lie inside the given buffers, and for
- * the paged call 0 <= block_table[b][i] < num_pages for i < ceil(ctx_lens[b]
- * / page_size). A sequence with q_lens[b] == 0 writes nothing; rows of other
- * sequences are never touched.
+ * argument returns its status with nothing enqueued. Device-side contract:
+ * 0 <= q_lens[b] <= ctx_lens[b] <= max_ctx_len, q_lens[b] <= max_q_len,
+ * contexts and query rows lie inside the given buffers, and for the paged
+ * call 0 <= block_table[b][i] < num_pages for i < ceil(ctx_lens[b] /
+ * page_size). The kernel clamps ctx_lens[b] into [0, max_ctx_len] and
+ * q_lens[b] into [0, min(ctx_lens[b], max_q_len)], and reads an entry outside
+ * [0, num_pages) as page 0, so a violation gives wrong rows for its sequence
+ * but no read outside the page pool; these calls have no workspace and record
+ * no error word (COMEM_FLAG_DEBUG_CHECKS does not apply). A sequence with
+ * q_lens[b] == 0 writes nothing; rows of other sequences are never touched.
  */
 #ifndef COMEM_PREFILL_ATTN_H
 #define COMEM_PREFILL_ATTN_H

@@ -30,8 +30,10 @@ EXPORTED = (
     "comem_decode_attn_init", "comem_decode_attn_destroy", "comem_status_string",
     "comem_decode_attn_plan_splits", "comem_decode_attn", "comem_decode_attn_paged",
     "comem_kv_append", "comem_kv_append_paged", "comem_append_decode_attn", "comem_append_decode_attn_paged",
-    "comem_prefill_attn", "comem_prefill_attn_paged",
+    "comem_prefill_attn", "comem_prefill_attn_paged", "comem_decode_attn_device_errors",
 )
+FLAG_DEBUG_CHECKS = 1
+DEVICE_ERR_CTX_LEN, DEVICE_ERR_BLOCK_TABLE = 1, 2
 PROBE_EXPORTED = ("comem_probe_read", "comem_probe_copy")
 COST_EXPORTED = (
     "comem_cost_kv_bytes_per_token", "comem_cost_decode_time", "comem_cost_decode_saving",
@@ -52,6 +54,7 @@ class Config(ctypes.Structure):
         ("variant", ctypes.c_int32),
         ("k_scale", ctypes.c_float),
         ("v_scale", ctypes.c_float),
+        ("flags", ctypes.c_uint32),
     ]
 
 
@@ -93,6 +96,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.comem_status_string.restype = ctypes.c_char_p
     lib.comem_decode_attn_plan_splits.argtypes = [vp, i32, i64, sz, ctypes.POINTER(i32), ctypes.POINTER(i32)]
     lib.comem_decode_attn_plan_splits.restype = ctypes.c_int
+    lib.comem_decode_attn_device_errors.argtypes = [vp, vp, sz, ctypes.POINTER(ctypes.c_uint32), vp]
+    lib.comem_decode_attn_device_errors.restype = ctypes.c_int
     lib.comem_decode_attn.argtypes = [vp, vp, vp, vp, i64, i64, vp, vp, i32, i64, vp, vp, vp, sz, vp]
     lib.comem_decode_attn.restype = ctypes.c_int
     lib.comem_decode_attn_paged.argtypes = [vp, vp, vp, vp, i64, i64, i64, i32, i64, vp, i32, vp, i32, i64,
@@ -180,6 +185,14 @@ def comem_decode_attn_init(cfg: Config, device: int) -> Tuple[int, int]:
 
 def comem_decode_attn_destroy(plan: int) -> None:
     _check(load_library().comem_decode_attn_destroy(plan), "comem_decode_attn_destroy")
+
+
+def comem_decode_attn_device_errors(plan: int, workspace: int, workspace_bytes: int, stream: Optional[int]) -> int:
+    """COMEM_DEVICE_ERR_* bits recorded by calls using this workspace since the last read (then cleared)."""
+    word = ctypes.c_uint32()
+    _check(load_library().comem_decode_attn_device_errors(plan, workspace, workspace_bytes, ctypes.byref(word),
+                                                          stream), "comem_decode_attn_device_errors")
+    return word.value
 
 
 def comem_decode_attn_plan_splits(plan: int, batch: int, max_ctx_len: int, workspace_bytes: int) -> Tuple[int, int]:
@@ -300,13 +313,14 @@ class DecodeAttention:
 
     def __init__(self, num_q_heads: int, num_kv_heads: int, head_dim: int, dtype: str, scale: float,
                  max_batch: int, max_ctx_len: int, chunk_tokens: int = 0, variant: str = "auto",
-                 device: int = 0, k_scale: float = 1.0, v_scale: float = 1.0):
+                 device: int = 0, k_scale: float = 1.0, v_scale: float = 1.0, debug_checks: bool = False):
         import torch
 
         self.cfg = Config(num_q_heads, num_kv_heads, head_dim, DTYPES[dtype], float(scale),
                           max_batch, max_ctx_len, chunk_tokens,
                           {"auto": VARIANT_AUTO, "valu": VARIANT_VALU, "mfma": VARIANT_MFMA,
-                           "mfma_grid": VARIANT_MFMA_GRID}[variant], float(k_scale), float(v_scale))
+                           "mfma_grid": VARIANT_MFMA_GRID}[variant], float(k_scale), float(v_scale),
+                          FLAG_DEBUG_CHECKS if debug_checks else 0)
         self.device = device
         self.plan, self.workspace_bytes = comem_decode_attn_init(self.cfg, device)
         self.workspace = torch.zeros(max(self.workspace_bytes, 256), dtype=torch.uint8, device=f"cuda:{device}")
@@ -324,6 +338,11 @@ class DecodeAttention:
 
     def splits(self, batch: int, max_ctx_len: int) -> Tuple[int, int]:
         return comem_decode_attn_plan_splits(self.plan, batch, max_ctx_len, self.workspace_bytes)
+
+    def device_errors(self, stream=None) -> int:
+        """Contract-violation bits (debug_checks=True) since the last read; waits for the stream."""
+        return comem_decode_attn_device_errors(self.plan, self.workspace.data_ptr(), self.workspace_bytes,
+                                               self._stream(stream))
 
     def _outputs(self, q, out, lse):
         import torch

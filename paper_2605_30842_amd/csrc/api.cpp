@@ -61,6 +61,20 @@ int elem_bytes(const comem_decode_attn_config& c) {
 }
 bool is_fp8(const comem_decode_attn_config& c) { return c.dtype == COMEM_FP8_E4M3; }
 
+// After the tickets [max_batch * Hkv]: the two work-queue counters and the
+// device error word.
+constexpr int kCounterWords = 3;
+constexpr int kErrorWord = 2;  // index after the tickets
+
+bool debug_checks(const comem_decode_attn_plan& p) { return (p.cfg.flags & COMEM_FLAG_DEBUG_CHECKS) != 0; }
+
+// With debug checks the error word lives in the workspace, so one is needed.
+comem_status check_debug_workspace(const comem_decode_attn_plan& p, const void* workspace, size_t ws_bytes) {
+  if (!debug_checks(p)) return COMEM_OK;
+  if (workspace == nullptr) return COMEM_ERR_NULL_POINTER;
+  return ws_bytes < p.ticket_bytes ? COMEM_ERR_WORKSPACE_TOO_SMALL : COMEM_OK;
+}
+
 // Workspace bytes for `slots` (sequence, split) partial results: ticket
 // counters, then per-head lse values, then per-head partial outputs.
 size_t slots_workspace_bytes(const comem_decode_attn_plan& p, int64_t slots) {
@@ -138,6 +152,7 @@ comem_status validate_config(const comem_decode_attn_config& c) {
   if (c.variant != COMEM_VARIANT_AUTO && c.variant != COMEM_VARIANT_VALU && c.variant != COMEM_VARIANT_MFMA &&
       c.variant != COMEM_VARIANT_MFMA_GRID)
     return COMEM_ERR_UNSUPPORTED;
+  if ((c.flags & ~COMEM_FLAG_DEBUG_CHECKS) != 0) return COMEM_ERR_UNSUPPORTED;
   if ((c.variant == COMEM_VARIANT_MFMA || c.variant == COMEM_VARIANT_MFMA_GRID) && c.dtype == COMEM_F32)
     return COMEM_ERR_UNSUPPORTED;
   if (c.dtype == COMEM_FP8_E4M3) {
@@ -275,10 +290,12 @@ comem_status launch_append(const comem::AppendParams& a, bool paged, int32_t bat
 
 void fill_common(const comem_decode_attn_plan& p, comem::AttnParams& a, const void* q, const void* k,
                  const void* v, int64_t stride_token, int64_t stride_head, const int32_t* ctx_lens,
-                 float* out, float* lse, void* workspace, int64_t batch, int64_t chunk, int64_t splits,
-                 bool queue) {
+                 float* out, float* lse, void* workspace, int64_t batch, int64_t max_ctx_len, int64_t chunk,
+                 int64_t splits, bool queue) {
   const int64_t e = elem_bytes(p.cfg);
   std::memset(&a, 0, sizeof(a));
+  a.max_ctx = static_cast<int32_t>(max_ctx_len);
+  if (debug_checks(p)) a.errors = static_cast<uint32_t*>(workspace) + p.cfg.max_batch * p.cfg.num_kv_heads + kErrorWord;
   a.q = static_cast<const char*>(q);
   a.k = static_cast<const char*>(k);
   a.v = static_cast<const char*>(v);
@@ -326,11 +343,13 @@ comem_status decode_contiguous(const comem_decode_attn_plan* plan, const void* q
   int64_t chunk = 0, splits = 0;
   st = plan_call(*p, batch, max_ctx_len, 0, workspace == nullptr ? 0 : workspace_bytes, &chunk, &splits);
   if (st != COMEM_OK) return st;
+  st = check_debug_workspace(*p, workspace, workspace_bytes);
+  if (st != COMEM_OK) return st;
   if (p->device == COMEM_NO_DEVICE) return COMEM_ERR_NO_DEVICE;
   const bool queue = uses_queue(*p, batch, workspace, workspace_bytes);
   comem::AttnParams a;
-  fill_common(*p, a, q, k, v, stride_token, stride_head, ctx_lens, out, lse, workspace, batch, chunk, splits,
-              queue);
+  fill_common(*p, a, q, k, v, stride_token, stride_head, ctx_lens, out, lse, workspace, batch, max_ctx_len, chunk,
+              splits, queue);
   a.seq_start = seq_start;
   if (fused) {
     a.new_k = static_cast<const char*>(new_k);
@@ -362,11 +381,13 @@ comem_status decode_paged(const comem_decode_attn_plan* plan, const void* q, con
   // The matrix-core kernel stages one split's block-table entries in LDS (a
   // planned split always fits; a configured chunk_tokens may not).
   if (uses_mfma(*p) && (chunk - 1) / page_size + 2 > comem::mfma_max_split_pages()) return COMEM_ERR_INVALID_SHAPE;
+  st = check_debug_workspace(*p, workspace, workspace_bytes);
+  if (st != COMEM_OK) return st;
   if (p->device == COMEM_NO_DEVICE) return COMEM_ERR_NO_DEVICE;
   const bool queue = uses_queue(*p, batch, workspace, workspace_bytes);
   comem::AttnParams a;
   fill_common(*p, a, q, k_pages, v_pages, stride_token, stride_head, ctx_lens, out, lse, workspace, batch,
-              chunk, splits, queue);
+              max_ctx_len, chunk, splits, queue);
   a.block_table = block_table;
   a.stride_page = stride_page * elem_bytes(p->cfg);
   a.max_pages = max_pages_per_seq;
@@ -408,6 +429,8 @@ comem_status prepare_prefill(const comem_decode_attn_plan& p, const void* q, con
   a.group = group_of(p.cfg);
   a.tokens_per_block = comem::kPrefillRows / a.group;
   a.scale_log2 = p.cfg.scale * 1.4426950408889634f;
+  a.max_ctx = static_cast<int32_t>(max_ctx_len);
+  a.max_q = max_q_len;
   return COMEM_OK;
 }
 
@@ -470,7 +493,7 @@ comem_status comem_decode_attn_init(const comem_decode_attn_config* cfg, int dev
   p->device = device;
   p->num_cus = num_cus > 0 ? num_cus : kAssumedCUs;
   // tickets (one per sequence and KV head), then the two work-queue counters
-  p->ticket_bytes = align256((static_cast<size_t>(cfg->max_batch) * cfg->num_kv_heads + 2) * 4);
+  p->ticket_bytes = align256((static_cast<size_t>(cfg->max_batch) * cfg->num_kv_heads + kCounterWords) * 4);
   // Largest number of (sequence, split) slots any call within the limits plans
   // (bounded for the matrix-core kernel by its smallest split of 1024 tokens);
   // calls with a smaller workspace get coarser splits.
@@ -499,6 +522,28 @@ comem_status comem_decode_attn_destroy(comem_decode_attn_plan* plan) {
   if (plan->magic != kPlanMagic) return COMEM_ERR_BAD_HANDLE;
   plan->magic = 0;
   delete plan;
+  return COMEM_OK;
+}
+
+comem_status comem_decode_attn_device_errors(const comem_decode_attn_plan* plan, void* workspace,
+                                             size_t workspace_bytes, uint32_t* errors_out, void* hip_stream) {
+  const comem_decode_attn_plan* p = checked(plan);
+  if (p == nullptr) return COMEM_ERR_BAD_HANDLE;
+  if (workspace == nullptr || errors_out == nullptr) return COMEM_ERR_NULL_POINTER;
+  if (!aligned(workspace, 256)) return COMEM_ERR_MISALIGNED;
+  if (workspace_bytes < p->ticket_bytes) return COMEM_ERR_WORKSPACE_TOO_SMALL;
+  *errors_out = 0;
+  if (p->device == COMEM_NO_DEVICE) return COMEM_ERR_NO_DEVICE;
+  hipStream_t s = static_cast<hipStream_t>(hip_stream);
+  uint32_t* word = static_cast<uint32_t*>(workspace) + p->cfg.max_batch * p->cfg.num_kv_heads + kErrorWord;
+  uint32_t host = 0;
+  if (hipMemcpyAsync(&host, word, sizeof(host), hipMemcpyDeviceToHost, s) != hipSuccess) return COMEM_ERR_HIP;
+  if (hipStreamSynchronize(s) != hipSuccess) return COMEM_ERR_HIP;
+  if (host != 0) {
+    if (hipMemsetAsync(word, 0, sizeof(host), s) != hipSuccess) return COMEM_ERR_HIP;
+    if (hipStreamSynchronize(s) != hipSuccess) return COMEM_ERR_HIP;
+  }
+  *errors_out = host;
   return COMEM_OK;
 }
 
@@ -602,6 +647,7 @@ comem_status comem_prefill_attn_paged(const comem_decode_attn_plan* plan, const 
   a.max_pages = max_pages_per_seq;
   a.page_shift = log2_of(page_size);
   a.page_mask = page_size - 1;
+  a.num_pages = num_pages;
   return launch_prefill(*p, a, true, batch, max_q_len, hip_stream);
 }
 

@@ -56,9 +56,34 @@ struct AttnParams {
   float* o_part;       // [B, Hkv, S, G, D]
   const char* new_k;   // fused append: new rows [B, Hkv, D], or nullptr for attention only
   const char* new_v;
-  int64_t num_pages;   // paged layout: pool size (bounds the fused append's store)
+  int64_t num_pages;   // paged layout: pool size (bounds every page access)
   float out_scale;     // multiplies every output (the V scale of an FP8 cache, else 1)
+  int32_t max_ctx;     // the call's max_ctx_len: lengths are clamped to [0, max_ctx]
+  uint32_t* errors;    // device error word (debug checks), or nullptr
 };
+
+// Device-side contract checks. A length outside [0, max_ctx] is clamped into
+// it; a block-table entry outside [0, num_pages) becomes -1, which reads use
+// as page 0 and stores skip. With an error word, each violation also sets its
+// bit there (the COMEM_DEVICE_ERR_* values of the C header).
+constexpr uint32_t kErrCtxLen = 1u;
+constexpr uint32_t kErrBlockTable = 2u;
+
+__device__ inline int checked_len(int L, int max_ctx, uint32_t* errors) {
+  if (L < 0 || L > max_ctx) {
+    if (errors != nullptr) atomicOr(errors, kErrCtxLen);
+    L = L < 0 ? 0 : max_ctx;
+  }
+  return L;
+}
+
+__device__ inline int32_t checked_page(int32_t page, int64_t num_pages, uint32_t* errors) {
+  if (page < 0 || page >= num_pages) {
+    if (errors != nullptr) atomicOr(errors, kErrBlockTable);
+    return -1;
+  }
+  return page;
+}
 
 // Per-wave partial state handed from the token loop to the finalize step.
 template <int D>
@@ -82,7 +107,8 @@ __device__ inline int uniform_i32(int x) {
 template <bool PAGED>
 __device__ inline int64_t row_offset(const AttnParams& p, int b, int64_t seq0, int t) {
   if constexpr (PAGED) {
-    const int page = p.block_table[static_cast<int64_t>(b) * p.max_pages + (t >> p.page_shift)];
+    const int page = max(0, checked_page(p.block_table[static_cast<int64_t>(b) * p.max_pages + (t >> p.page_shift)],
+                                         p.num_pages, p.errors));
     return static_cast<int64_t>(page) * p.stride_page +
            static_cast<int64_t>(t & p.page_mask) * p.stride_token;
   } else {
@@ -117,7 +143,8 @@ __device__ inline void store_new_token(const AttnParams& p, int b, int hk, int64
 // Paged layout: byte offset of the page slot of token t, or -1 when the
 // block-table entry lies outside the pool.
 __device__ inline int64_t checked_page_row(const AttnParams& p, int32_t page, int t) {
-  if (page < 0 || page >= p.num_pages) return -1;
+  page = checked_page(page, p.num_pages, p.errors);
+  if (page < 0) return -1;
   return static_cast<int64_t>(page) * p.stride_page + static_cast<int64_t>(t & p.page_mask) * p.stride_token;
 }
 

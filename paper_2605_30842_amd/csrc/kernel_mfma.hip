@@ -174,7 +174,7 @@ struct Loader {
     if constexpr (LAYOUT == Layout::kContig) {
       return static_cast<int64_t>(t) * stride_token;
     } else {
-      const int page = sm_pages[(t - page_first) >> page_shift];
+      const int page = max(0, sm_pages[(t - page_first) >> page_shift]);  // -1 (outside the pool) reads page 0
       return static_cast<int64_t>(page) * stride_page + static_cast<int64_t>(t & page_mask) * stride_token;
     }
   }
@@ -331,6 +331,7 @@ __device__ inline void load_sequence(const AttnParams& p, int b, int& L, int64_t
   L = uniform_i32(p.ctx_lens[b]);
   seq_row = LAYOUT == Layout::kContig ? uniform_i64(p.seq_start[b]) : 0;
   asm volatile("" : "+s"(L), "+s"(seq_row));
+  L = checked_len(L, p.max_ctx, p.errors);
 }
 
 // Shared memory of one workgroup; the page table and the wave states are
@@ -378,7 +379,7 @@ __device__ void attend_split(const AttnParams& p, SplitSmem<D, LAYOUT>& sm, int 
     const int first = t_begin >> p.page_shift;
     const int count = ((t_end - 1) >> p.page_shift) - first + 1;
     const int32_t* row = p.block_table + static_cast<int64_t>(b) * p.max_pages + first;
-    for (int i = threadIdx.x; i < count; i += kThreads) sm.pages[i] = row[i];
+    for (int i = threadIdx.x; i < count; i += kThreads) sm.pages[i] = checked_page(row[i], p.num_pages, p.errors);
     __syncthreads();
   }
   ld.sm_pages = sm.pages;
@@ -413,8 +414,9 @@ __device__ void attend_split(const AttnParams& p, SplitSmem<D, LAYOUT>& sm, int 
   const int ntok = t_end - t_begin;
   const int nfull = ntok >> 5;              // full 32-token tiles
   const int ntiles = (ntok + 31) >> 5;      // including a partial last tile
-  // Fused append: the wave that owns the tile of token L - 1 stores its rows first.
-  if (p.new_k != nullptr && t_end == L && L > 0 && w == (ntiles - 1) % kWaves) {
+  // Fused append: the wave that owns the tile of token L - 1 stores its rows
+  // first (not when the length was clamped: that row is not the new token's).
+  if (p.new_k != nullptr && t_end == L && L > 0 && w == (ntiles - 1) % kWaves && p.ctx_lens[b] == L) {
     int64_t row;
     if constexpr (LAYOUT == Layout::kContig) {
       row = (seq_row + static_cast<int64_t>(L - 1)) * p.stride_token;
@@ -519,7 +521,7 @@ __global__ __launch_bounds__(kThreads, 2) void decode_mfma_queue_kernel(const At
 
   // Splits per sequence, then an exclusive prefix sum (one wave scans).
   for (int b = tid; b < batch; b += kThreads) {
-    const int L = p.ctx_lens[b];
+    const int L = checked_len(p.ctx_lens[b], p.max_ctx, nullptr);  // reported by load_sequence
     sm_first[b + 1] = L > 0 ? 1 + (L - 1) / p.chunk : 1;
   }
   __syncthreads();

@@ -118,6 +118,7 @@ struct TileLoader {
   const int32_t* bt_row;  // block-table row of the sequence (paged)
   int64_t stride_token;
   int64_t stride_page;
+  int64_t num_pages;
   int page_shift, page_mask;
   int kend;  // keys [0, kend) are needed
   int w, lane;
@@ -144,13 +145,16 @@ struct TileLoader {
 
   __device__ int fine_key(int t0, int u) const { return min(t0 + 16 * w + RPI * u + lane / CH, kend - 1); }
 
+  // A block-table entry outside the pool reads page 0.
+  __device__ int32_t in_pool(int32_t page) const { return page < 0 || page >= num_pages ? 0 : page; }
+
   __device__ void fetch_pages(int t0) {
     if constexpr (LAYOUT == PLayout::kPaged) {
       const int g0 = t0 + 16 * w;
-      page = g0 < kend ? bt_row[g0 >> page_shift] : 0;
+      page = g0 < kend ? in_pool(bt_row[g0 >> page_shift]) : 0;
     } else if constexpr (LAYOUT == PLayout::kPagedFine) {
 #pragma unroll
-      for (int u = 0; u < NI; ++u) fine_page[u] = bt_row[fine_key(t0, u) >> page_shift];
+      for (int u = 0; u < NI; ++u) fine_page[u] = in_pool(bt_row[fine_key(t0, u) >> page_shift]);
     }
   }
 
@@ -348,7 +352,8 @@ __global__ __launch_bounds__(kPrefillThreads, 2) void prefill_mfma_kernel(const 
   int64_t qs = p.q_start[b];
   int64_t seq0 = PAGED ? 0 : p.seq_start[b];
   asm volatile("" : "+s"(L), "+s"(M), "+s"(qs), "+s"(seq0));  // one round trip for all four
-  M = min(M, L);
+  L = min(max(L, 0), p.max_ctx);
+  M = min(max(M, 0), min(L, p.max_q));
   // q counts from each sequence's last (heaviest) block of new tokens.
   const int nblk = (M + TB - 1) / TB;
   if (q >= nblk) return;
@@ -374,6 +379,7 @@ __global__ __launch_bounds__(kPrefillThreads, 2) void prefill_mfma_kernel(const 
   ld.bt_row = PAGED ? p.block_table + static_cast<int64_t>(b) * p.max_pages : nullptr;
   ld.stride_token = p.stride_token;
   ld.stride_page = p.stride_page;
+  ld.num_pages = p.num_pages;
   ld.page_shift = p.page_shift;
   ld.page_mask = p.page_mask;
   ld.kend = kend;

@@ -48,7 +48,7 @@ __global__ __launch_bounds__(kThreads) void decode_valu_kernel(const AttnParams 
   constexpr int U = 4;            // loads per lane per tile
   constexpr int TT = RPL * U;     // tokens per tile
   const int j = blockIdx.x, hk = blockIdx.y, b = blockIdx.z;
-  const int L = p.ctx_lens[b];
+  const int L = checked_len(p.ctx_lens[b], p.max_ctx, p.errors);
   const int nsplit_b = L > 0 ? 1 + (L - 1) / p.chunk : 1;
   if (j >= nsplit_b) return;
   const int t_begin = j * p.chunk;
@@ -84,8 +84,9 @@ __global__ __launch_bounds__(kThreads) void decode_valu_kernel(const AttnParams 
 
   const int ntok = t_end - t_begin;
   // Fused append: the wave whose tile holds token L - 1 (and every clamped
-  // read of that row) stores the new rows first.
-  if (p.new_k != nullptr && t_end == L && L > 0 && w == ((L - 1 - t_begin) / TT) % kWaves) {
+  // read of that row) stores the new rows first (not when the length was
+  // clamped: that row is not the new token's).
+  if (p.new_k != nullptr && t_end == L && L > 0 && w == ((L - 1 - t_begin) / TT) % kWaves && p.ctx_lens[b] == L) {
     int64_t row;
     if constexpr (PAGED) {
       row = checked_page_row(p, p.block_table[static_cast<int64_t>(b) * p.max_pages + ((L - 1) >> p.page_shift)],

@@ -32,6 +32,9 @@ struct PrefillParams {
   int32_t group;               // G = Hq / Hkv
   int32_t tokens_per_block;    // kPrefillRows / G new tokens per workgroup
   float scale_log2;            // scale * log2(e)
+  int32_t max_ctx;             // ctx_lens[b] is clamped to [0, max_ctx]
+  int32_t max_q;               // q_lens[b] is clamped to [0, min(L_b, max_q)]
+  int64_t num_pages;           // paged layout: entries outside [0, num_pages) read page 0
 };
 
 using PrefillKernelFn = void (*)(PrefillParams);

@@ -47,13 +47,13 @@ class DeviceWorkload:
             self.seq_start = torch.from_numpy(w.seq_start.astype(np.int64)).to(device)
 
 
-def make_op(spec, chunk=0, variant="auto", max_batch=None, max_ctx_len=None):
+def make_op(spec, chunk=0, variant="auto", max_batch=None, max_ctx_len=None, debug_checks=False):
     from paper_2605_30842_amd.binding import DecodeAttention
 
     scales = dict(k_scale=spec.k_scale, v_scale=spec.v_scale) if spec.dtype == "fp8" else {}
     return DecodeAttention(spec.num_q_heads, spec.num_kv_heads, spec.head_dim, spec.dtype, float(spec.scale),
                            max_batch or spec.batch, max_ctx_len or spec.max_ctx_len, chunk_tokens=chunk,
-                           variant=variant, **scales)
+                           variant=variant, debug_checks=debug_checks, **scales)
 
 
 def run(dw: DeviceWorkload, op, want_lse=True, max_ctx_len=None):

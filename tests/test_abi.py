@@ -220,6 +220,43 @@ def test_configured_split_too_long_for_the_page_table_copy():
         B.comem_decode_attn_destroy(p)
 
 
+def test_flags_validation():
+    assert _status_init(_cfg(flags=2)) == B.ERR_UNSUPPORTED
+    assert _status_init(_cfg(flags=B.FLAG_DEBUG_CHECKS)) == B.OK
+
+
+def test_debug_checks_need_a_workspace_on_the_host():
+    """With COMEM_FLAG_DEBUG_CHECKS the error word lives in the workspace: a call without one is refused
+    before anything is launched (a plan without a device then stops at the device)."""
+    p, ws = B.comem_decode_attn_init(_cfg(flags=B.FLAG_DEBUG_CHECKS), B.NO_DEVICE)
+    try:
+        assert _call(_contig_args(p, ws, max_ctx_len=64)) == B.ERR_NO_DEVICE
+        assert _call(_contig_args(p, ws, max_ctx_len=64, workspace=None, workspace_bytes=0)) == B.ERR_NULL_POINTER
+        assert _call(_contig_args(p, ws, max_ctx_len=64, workspace_bytes=64)) == B.ERR_WORKSPACE_TOO_SMALL
+        args = _paged_args(p, ws, workspace=None, workspace_bytes=0, max_ctx_len=64)
+        assert B.load_library().comem_decode_attn_paged(*args.values()) == B.ERR_NULL_POINTER
+    finally:
+        B.comem_decode_attn_destroy(p)
+    p, ws = B.comem_decode_attn_init(_cfg(), B.NO_DEVICE)
+    try:  # without the flag a short call needs no workspace at all
+        assert _call(_contig_args(p, ws, max_ctx_len=64, workspace=None, workspace_bytes=0)) == B.ERR_NO_DEVICE
+    finally:
+        B.comem_decode_attn_destroy(p)
+
+
+def test_device_errors_validation(plan):
+    p, ws = plan
+    lib = B.load_library()
+    word = ctypes.c_uint32(7)
+    assert lib.comem_decode_attn_device_errors(None, A, ws, ctypes.byref(word), None) == B.ERR_BAD_HANDLE
+    assert lib.comem_decode_attn_device_errors(p, None, ws, ctypes.byref(word), None) == B.ERR_NULL_POINTER
+    assert lib.comem_decode_attn_device_errors(p, A, ws, None, None) == B.ERR_NULL_POINTER
+    assert lib.comem_decode_attn_device_errors(p, A + 16, ws, ctypes.byref(word), None) == B.ERR_MISALIGNED
+    assert lib.comem_decode_attn_device_errors(p, A, 16, ctypes.byref(word), None) == B.ERR_WORKSPACE_TOO_SMALL
+    assert lib.comem_decode_attn_device_errors(p, A, ws, ctypes.byref(word), None) == B.ERR_NO_DEVICE
+    assert word.value == 0
+
+
 def _append_args(plan, **kw):
     args = dict(plan=plan, new_k=A, new_v=A, k=A, v=A, stride_token=8 * 128, stride_head=128, seq_start=A,
                 ctx_lens=A, batch=2, max_ctx_len=4096, stream=None)
