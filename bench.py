@@ -37,6 +37,9 @@ KERNEL_SOURCES = ["paper_2605_30842_amd/csrc/api.cpp", "paper_2605_30842_amd/csr
                   "paper_2605_30842_amd/csrc/kernel_mfma.hip", "paper_2605_30842_amd/csrc/kernel_valu.hip"]
 PREFILL_SOURCES = ["paper_2605_30842_amd/csrc/api.cpp", "paper_2605_30842_amd/csrc/attn_common.h",
                    "paper_2605_30842_amd/csrc/prefill.h", "paper_2605_30842_amd/csrc/kernel_prefill.hip"]
+APPEND_SOURCES = ["paper_2605_30842_amd/csrc/api.cpp", "paper_2605_30842_amd/csrc/kv_append.h",
+                  "paper_2605_30842_amd/csrc/kernel_append.hip"]
+APPEND_PROFILED = (2, 5)  # decode workloads whose standalone append is traced (contiguous, paged)
 COPY_CAL_BYTES = 256 << 20  # size of the copy used to calibrate FETCH_SIZE / WRITE_SIZE
 METRIC = "decode-attention effective HBM GB/s (% of peak) and µs/step at 32k-128k ctx"
 MALL_BYTES = 256 << 20
@@ -170,7 +173,7 @@ def _short_kernel_name(full):
     """
     import re
 
-    m = re.search(r"((?:decode|prefill)_\w+?)(?:_kernel)?<([^>]*)>", full)
+    m = re.search(r"((?:decode|prefill)_\w+?|kv_append)(?:_kernel)?<([^>]*)>", full)
     if not m:
         return re.sub(r"\W+", "_", full.split("<")[0]).strip("_")[:60]
     base, args = m.group(1), m.group(2)
@@ -217,14 +220,22 @@ def summarize(a):
     fetch_scale = COPY_CAL_BYTES / 1024 / cal_f if cal_f else None
     write_scale = COPY_CAL_BYTES / 1024 / cal_w if cal_w else None
     os.makedirs(PROFILES, exist_ok=True)
-    jobs = [("w", i, spec) for i, spec in WORKLOADS.items()] + [("p", i, spec) for i, spec in PREFILL_WORKLOADS.items()]
+    jobs = ([("w", i, spec) for i, spec in WORKLOADS.items()] +
+            [("p", i, spec) for i, spec in PREFILL_WORKLOADS.items()] +
+            [("a", i, WORKLOADS[i]) for i in APPEND_PROFILED])
     for tag, i, spec in jobs:
         stats = _kernel_stats(os.path.join(d, "prof", f"{tag}{i}"))
         if not stats:
             continue
-        key = "decode_" if tag == "w" else "prefill_"
+        key = {"w": "decode_", "p": "prefill_", "a": "kv_append"}[tag]
         attn = [r for r in stats if key in r["Name"]]
-        if tag == "w":
+        if tag == "a":
+            # K and V rows of every (sequence, KV head): read from the inputs, written to the cache
+            units = {"moved_bytes": 2 * 2 * spec.batch * spec.num_kv_heads * spec.head_dim * spec.elem_bytes}
+            sources = APPEND_SOURCES
+            bench_args = f"--workload {i} --op append --cpu-seconds 0"
+            pmc_args = None
+        elif tag == "w":
             w = generate(spec)
             units = {"algorithmic_bytes": w.kv_bytes}
             sources = KERNEL_SOURCES
@@ -246,7 +257,10 @@ def summarize(a):
         rec = {"workload": spec.name, "kernel": kname, "kernel_source_hash": kernel_source_hash(sources),
                "calls": int(attn[0]["Calls"]) if attn else 0, "avg_duration_us": avg_ns / 1e3 if avg_ns else None}
         rec.update(units)
-        if tag == "w":
+        if tag == "a":
+            kv = units["moved_bytes"]
+            rec["achieved_GBps_from_trace"] = round(kv / avg_ns, 3) if avg_ns else None
+        elif tag == "w":
             kv = units["algorithmic_bytes"]
             rec["achieved_GBps_from_trace"] = round(kv / avg_ns, 1) if avg_ns else None
         else:
@@ -263,7 +277,7 @@ def summarize(a):
                     " and returning to the root):\n\n```\n")
             f.write(f"rocprofv3 --kernel-trace --stats --output-format csv -d {d}/prof/{tag}{i} -o {tag}{i} -- "
                     f"python3 bench.py {bench_args}\n")
-            for c in ("FETCH_SIZE", "WRITE_SIZE"):
+            for c in ("FETCH_SIZE", "WRITE_SIZE") if pmc_args else ():
                 sub = "fetch" if c == "FETCH_SIZE" else "write"
                 f.write(f"rocprofv3 --pmc {c} --output-format csv -d {d}/pmc/{tag}{i}_{sub} -o {tag}{i}_{sub} -- "
                         f"python3 bench.py {pmc_args}\n")
@@ -279,8 +293,12 @@ def summarize(a):
             for r in stats:
                 f.write(f"| {_short_kernel_name(r['Name'])} | {r['Calls']} | {float(r['AverageNs'])/1e3:.2f} | "
                         f"{float(r['MinNs'])/1e3:.2f} | {float(r['MaxNs'])/1e3:.2f} |\n")
-            f.write("\nHBM traffic per dispatch: FETCH_SIZE and WRITE_SIZE medians (KiB), each scaled by the factor "
-                    f"that makes the same counter read {COPY_CAL_BYTES} bytes for a copy of that size.\n\n")
+            if pmc_args:
+                f.write("\nHBM traffic per dispatch: FETCH_SIZE and WRITE_SIZE medians (KiB), each scaled by the "
+                        f"factor that makes the same counter read {COPY_CAL_BYTES} bytes for a copy of that size.\n\n")
+            else:
+                f.write("\nA few KB per dispatch: the kernel is bound by launch latency, so no traffic counters were "
+                        "taken.\n\n")
             f.write("```json\n" + json.dumps(rec, indent=1) + "\n```\n")
             if counters:
                 f.write("\nCounters (medians over the kernel's dispatches in the --pmc runs above; percentages as "
