@@ -1,0 +1,90 @@
+"""The largest shapes the C ABI accepts, against the oracle.
+
+- A context of 1.1M tokens whose token rows are 4 KB apart (one KV head in a
+  16-head-wide buffer), so byte offsets pass 4 GiB: every offset on the path
+  must be 64-bit.
+- Batches at the work queue's limit (4096 sequences), one past it (the
+  one-workgroup-per-split grid takes over) and at the grid's limit (65535).
+"""
+
+import numpy as np
+import pytest
+
+import oracle.decode_attention as da
+from tests.gpu_util import DeviceWorkload, check, make_op, run, say, to_torch
+from workloads.synth import WORKLOADS, generate, small_spec
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _cuda():
+    import torch
+
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    from paper_2605_30842_amd import binding
+
+    binding.load_library()
+    yield
+
+
+@pytest.fixture(scope="module")
+def long_case():
+    spec = small_spec(WORKLOADS[2], [1_100_000], seed=90).replace(num_q_heads=8, num_kv_heads=1)
+    w = generate(spec)
+    return spec, w, *da.reference(w)
+
+
+@pytest.mark.parametrize("variant", ["mfma", "valu"])
+def test_byte_offsets_beyond_4_gib(long_case, variant):
+    import torch
+
+    spec, w, ro, rl = long_case
+    T = w.k.shape[0]
+    say(f"limits: {T} tokens at a 4 KB token stride, {variant}")
+    k_big = torch.zeros((T, 16, 128), dtype=torch.bfloat16, device="cuda:0")
+    v_big = torch.zeros_like(k_big)
+    k, v = k_big[:, :1, :], v_big[:, :1, :]
+    k.copy_(to_torch(w.k, "bf16", "cuda:0"))
+    v.copy_(to_torch(w.v, "bf16", "cuda:0"))
+    assert k.stride(0) * 2 * (T - 1) > 2 ** 32
+    q = to_torch(w.q, "bf16", "cuda:0")
+    ss = torch.zeros(1, dtype=torch.int64, device="cuda:0")
+    cl = torch.full((1,), T, dtype=torch.int32, device="cuda:0")
+    op = make_op(spec, variant=variant)
+    lse = torch.empty((1, spec.num_q_heads), dtype=torch.float32, device="cuda:0")
+    out, lse = op.forward(q, k, v, ss, cl, spec.max_ctx_len, lse=lse)
+    torch.cuda.synchronize()
+    check(out.cpu().numpy(), lse.cpu().numpy(), ro, rl, "bf16", f"4 GiB offsets {variant}")
+    del k_big, v_big, k, v
+    torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("variant", ["mfma", "valu"])
+@pytest.mark.parametrize("B", [4096, 4097])
+def test_batches_at_the_work_queue_limit(B, variant):
+    lens = np.random.default_rng(92 + B).integers(0, 65, size=B).tolist()
+    spec = small_spec(WORKLOADS[2], lens, seed=93)
+    w = generate(spec)
+    say(f"limits: batch {B}, {variant}")
+    out, lse = run(DeviceWorkload(w), make_op(spec, variant=variant))
+    ro, rl = da.reference(w)
+    check(out, lse, ro, rl, "bf16", f"batch {B} {variant}")
+
+
+def test_batch_at_the_grid_limit():
+    B = 65535
+    lens = np.random.default_rng(94).integers(0, 4, size=B)
+    spec = small_spec(WORKLOADS[2], lens.tolist(), seed=95)
+    w = generate(spec)
+    say(f"limits: batch {B}")
+    out, lse = run(DeviceWorkload(w), make_op(spec))
+    empty = lens == 0
+    assert np.all(out[empty] == 0) and np.all(lse[empty] == -np.inf)
+    assert np.all(np.isfinite(out)) and np.all(np.isfinite(lse[~empty]))
+    r = np.random.default_rng(96)
+    rows = sorted({(0, 0), (B - 1, spec.num_q_heads - 1),
+                   *[(int(r.integers(B)), int(r.integers(spec.num_q_heads))) for _ in range(60)]})
+    ref = da.decode_attention_rows(w, rows)
+    check(np.stack([out[b, h] for b, h in rows]), np.array([lse[b, h] for b, h in rows]),
+          np.stack([o for o, _ in ref]), np.array([l for _, l in ref]), "bf16", f"batch {B} sampled rows")
