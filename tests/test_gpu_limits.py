@@ -1,8 +1,8 @@
 """The largest shapes the C ABI accepts, against the oracle.
 
-- A context of 1.1M tokens whose token rows are 4 KB apart (one KV head in a
-  16-head-wide buffer), so byte offsets pass 4 GiB: every offset on the path
-  must be 64-bit.
+- Contexts whose byte offsets pass 4 GiB (one KV head in a buffer 16 or 32
+  heads wide): every offset on the path must be 64-bit. Decode over 1.1M
+  tokens is checked in full, prefill over 600K tokens on sampled rows.
 - Batches at the work queue's limit (4096 sequences), one past it (the
   one-workgroup-per-split grid takes over) and at the grid's limit (65535).
 """
@@ -11,8 +11,9 @@ import numpy as np
 import pytest
 
 import oracle.decode_attention as da
-from tests.gpu_util import DeviceWorkload, check, make_op, run, say, to_torch
-from workloads.synth import WORKLOADS, generate, small_spec
+import oracle.prefill_attention as pa
+from tests.gpu_util import DeviceWorkload, abs_values, check, check_prefill, make_op, run, say, to_torch
+from workloads.synth import PREFILL_WORKLOADS, WORKLOADS, generate, generate_prefill, small_prefill_spec, small_spec
 
 pytestmark = pytest.mark.gpu
 
@@ -88,3 +89,38 @@ def test_batch_at_the_grid_limit():
     ref = da.decode_attention_rows(w, rows)
     check(np.stack([out[b, h] for b, h in rows]), np.array([lse[b, h] for b, h in rows]),
           np.stack([o for o, _ in ref]), np.array([l for _, l in ref]), "bf16", f"batch {B} sampled rows")
+
+
+def test_prefill_byte_offsets_beyond_4_gib():
+    import torch
+
+    spec = small_prefill_spec(PREFILL_WORKLOADS[1], [600_000], [256], seed=97)
+    spec = spec.__class__(spec.name, spec.kv.replace(num_q_heads=8, num_kv_heads=1), spec.new_tokens, spec.seed)
+    pw = generate_prefill(spec)
+    w, s = pw.kv, pw.kv.spec
+    T = w.k.shape[0]
+    say(f"limits: prefill of 256 new tokens over {T} at an 8 KB token stride")
+    k_big = torch.zeros((T, 32, 128), dtype=torch.bfloat16, device="cuda:0")
+    v_big = torch.zeros_like(k_big)
+    k, v = k_big[:, :1, :], v_big[:, :1, :]
+    k.copy_(to_torch(w.k, "bf16", "cuda:0"))
+    v.copy_(to_torch(w.v, "bf16", "cuda:0"))
+    q = to_torch(pw.q, "bf16", "cuda:0")
+    q_start = torch.from_numpy(pw.q_start.astype(np.int64)).to("cuda:0")
+    q_lens = torch.from_numpy(pw.q_lens.astype(np.int32)).to("cuda:0")
+    ss = torch.zeros(1, dtype=torch.int64, device="cuda:0")
+    cl = torch.full((1,), T, dtype=torch.int32, device="cuda:0")
+    assert k.stride(0) * 2 * (T - 1) > 2 ** 32
+    lse = torch.empty((256, s.num_q_heads), dtype=torch.float32, device="cuda:0")
+    out, lse = make_op(s).prefill(q, q_start, q_lens, 256, k, v, ss, cl, s.max_ctx_len, lse=lse)
+    torch.cuda.synchronize()
+    out, lse = out.cpu().numpy(), lse.cpu().numpy()
+    del k_big, v_big, k, v
+    torch.cuda.empty_cache()
+    r = np.random.default_rng(98)
+    rows = sorted({(0, 0, 0), (0, 255, 7), *[(0, int(r.integers(256)), int(r.integers(8))) for _ in range(10)]})
+    ref = pa.prefill_attention_rows(pw, rows)
+    ref_abs = pa.prefill_attention_rows(abs_values(pw), rows)
+    check_prefill(np.stack([out[i, h] for _, i, h in rows]), np.array([lse[i, h] for _, i, h in rows]),
+                  np.stack([o for o, _ in ref]), np.array([l for _, l in ref]), np.stack([o for o, _ in ref_abs]),
+                  "prefill 4 GiB offsets")
