@@ -62,6 +62,35 @@ def test_byte_offsets_beyond_4_gib(long_case, variant):
 
 
 @pytest.mark.parametrize("variant", ["mfma", "valu"])
+def test_page_pool_beyond_4_gib(variant):
+    """8200 pages of 64 tokens, one KV head in a 32-head-wide pool (512 KB per page): pages past the
+    8192nd start beyond 4 GiB; a random block table reaches them."""
+    import torch
+
+    spec = small_spec(WORKLOADS[5], [8200 * 64], seed=99).replace(num_q_heads=8, num_kv_heads=1)
+    w = generate(spec)
+    P, ps = w.k_pages.shape[:2]
+    say(f"limits: paged pool of {P} pages x {ps} tokens at an 8 KB token stride, {variant}")
+    k_big = torch.zeros((P, ps, 32, 128), dtype=torch.bfloat16, device="cuda:0")
+    v_big = torch.zeros_like(k_big)
+    k, v = k_big[:, :, :1, :], v_big[:, :, :1, :]
+    k.copy_(to_torch(w.k_pages, "bf16", "cuda:0"))
+    v.copy_(to_torch(w.v_pages, "bf16", "cuda:0"))
+    assert k.stride(0) * 2 * (P - 1) > 2 ** 32
+    q = to_torch(w.q, "bf16", "cuda:0")
+    bt = torch.from_numpy(w.block_table.astype(np.int32)).to("cuda:0")
+    cl = torch.from_numpy(w.ctx_lens.astype(np.int32)).to("cuda:0")
+    lse = torch.empty((1, spec.num_q_heads), dtype=torch.float32, device="cuda:0")
+    out, lse = make_op(spec, variant=variant).forward_paged(q, k, v, bt, cl, spec.max_ctx_len, lse=lse)
+    torch.cuda.synchronize()
+    out, lse = out.cpu().numpy(), lse.cpu().numpy()
+    del k_big, v_big, k, v
+    torch.cuda.empty_cache()
+    ro, rl = da.reference(w)
+    check(out, lse, ro, rl, "bf16", f"paged pool past 4 GiB {variant}")
+
+
+@pytest.mark.parametrize("variant", ["mfma", "valu"])
 @pytest.mark.parametrize("B", [4096, 4097])
 def test_batches_at_the_work_queue_limit(B, variant):
     lens = np.random.default_rng(92 + B).integers(0, 65, size=B).tolist()
