@@ -138,7 +138,11 @@ const char* comem_status_string(comem_status status);
  * pages of 1 or 2 tokens may plan shorter splits, so that the block-table
  * entries of one split fit the matrix-core kernel's on-chip copy (2048
  * entries); a configured chunk_tokens that does not fit is refused with
- * COMEM_ERR_INVALID_SHAPE. */
+ * COMEM_ERR_INVALID_SHAPE. A sequence of L tokens has ceil(L / chunk)
+ * splits. When the matrix-core kernel's work queue has several rounds of
+ * work items and the chunk was planned (chunk_tokens = 0), a sequence's last
+ * splits are half a chunk each and the others up to 1.25 chunk; the split
+ * boundaries depend only on L and the plan, so results stay reproducible. */
 comem_status comem_decode_attn_plan_splits(const comem_decode_attn_plan* plan, int32_t batch,
                                            int64_t max_ctx_len, size_t workspace_bytes,
                                            int32_t* chunk_tokens_out, int32_t* num_splits_out);

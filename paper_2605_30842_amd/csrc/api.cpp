@@ -30,6 +30,7 @@ constexpr uint64_t kPlanMagic = 0x434f4d454d444131ull;  // "COMEMDA1"
 constexpr int kAssumedCUs = 256;                        // gfx950 (MI355X) without a device query
 constexpr int64_t kTargetWgsPerCu = 2;                  // workgroups per compute unit for one full round
 constexpr int kQueueWgsPerCu = 2;                       // resident workgroups per compute unit (MFMA kernel)
+constexpr int64_t kTailRounds = 4;                      // items per resident workgroup that enable short last splits
 constexpr int64_t kMinChunk = 64;                       // tokens per split, lower bound
 constexpr int64_t kMaxChunk = 2048;                     // tokens per split, upper bound (auto plan)
 constexpr int64_t kMaxContext = int64_t{1} << 30;
@@ -91,12 +92,14 @@ size_t call_workspace_bytes(const comem_decode_attn_plan& p, int64_t batch, int6
 // Tokens per split for the matrix-core kernel, from the host-side bounds of
 // a call (the device-side lengths are never read on the host). Splits of
 // 4096 tokens keep contexts of 128k and more at <= 32 splits; otherwise 2048
-// if that still leaves >= 8 work items per resident workgroup (so the work
-// queue can balance them), else 1024.
+// if that still leaves >= 16 work items per resident workgroup, else 1024.
+// Smaller items end the work queue more evenly (the last items handed out
+// finish at nearly the same time) at the cost of one more partial result
+// per item; at 8 items of 2048 tokens per workgroup the even end still wins.
 int64_t mfma_chunk(const comem_decode_attn_plan& p, int64_t batch, int64_t L) {
   if (L >= 32 * 4096) return 4096;
   const int64_t resident = static_cast<int64_t>(kQueueWgsPerCu) * p.num_cus;
-  if (batch * p.cfg.num_kv_heads * ceil_div(L, 2048) >= 8 * resident) return 2048;
+  if (batch * p.cfg.num_kv_heads * ceil_div(L, 2048) >= 16 * resident) return 2048;
   return 1024;
 }
 
@@ -230,6 +233,17 @@ comem_status launch(const comem_decode_attn_plan& p, bool paged, comem::AttnPara
   if (queue && items > resident) {
     comem::QueueKernelFn qfn = comem::select_mfma_queue_kernel(p.cfg.head_dim, paged, a.page_mask + 1, is_fp8(p.cfg));
     if (qfn == nullptr) return COMEM_ERR_UNSUPPORTED;
+    // With several rounds of items, each sequence ends in short splits of
+    // half a chunk, about one round of them in all: the queue hands them out
+    // last, so the workgroups finish closer together (quarter-chunk splits or
+    // two rounds of them gained less). Only planned chunks of 1024 tokens or
+    // more (and, paged, whose 1.25-chunk splits still fit the kernel's LDS
+    // copy of the block table); a configured chunk_tokens keeps even splits.
+    if (p.cfg.chunk_tokens == 0 && items >= kTailRounds * resident && a.chunk >= 1024 &&
+        (!paged || 2 * static_cast<int64_t>(a.chunk) <= mfma_page_cap(a.page_mask + 1))) {
+      a.tail_chunk = a.chunk / 2;
+      a.tail_splits = static_cast<int32_t>(ceil_div(resident, batch * p.cfg.num_kv_heads));
+    }
     dim3 grid(static_cast<unsigned>(items < resident ? items : resident));
     dim3 block(comem::kThreads);
     int nb = static_cast<int>(batch);

@@ -48,7 +48,9 @@ struct AttnParams {
   int32_t num_kv_heads;
   int32_t group;       // G = Hq / Hkv
   int32_t chunk;       // tokens per split (multiple of 32)
-  int32_t num_splits;  // gridDim.x
+  int32_t num_splits;  // most splits of one sequence (the stride of the partial results)
+  int32_t tail_chunk;  // work-queue form: tokens of each short last split, or 0 for none
+  int32_t tail_splits; // work-queue form: short last splits per sequence (at most a quarter of its splits)
   float scale_log2;    // scale * log2(e)
   uint32_t* tickets;   // [max_batch * Hkv] tickets, then 2 queue counters; zero between calls
   int32_t queue_slot;  // index of the queue counters in tickets

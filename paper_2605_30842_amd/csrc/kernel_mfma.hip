@@ -342,25 +342,63 @@ struct SplitSmem {
   int32_t pages[LAYOUT == Layout::kContig ? 1 : kMaxSplitPages];
 };
 
-// Attention of the G query heads of KV head hk of sequence b over split j
-// (tokens [j * chunk, min((j + 1) * chunk, L))), ending with this split's
-// share of the log-sum-exp merge. Called by every thread of the workgroup.
-// seq_row is seq_start[b] for the contiguous layout (unused when paged); the
-// callers load it together with ctx_lens[b], so the two loads cost one
-// round trip before the first tile is requested.
+// The splits of a sequence of L tokens. There are ceil(L / chunk) of them
+// (one, empty, when L = 0), normally split j = tokens [j * chunk, min((j + 1)
+// * chunk, L)). With short last splits (tail_chunk > 0: work-queue form),
+// the last `small` splits, at most a quarter of them, cover tail_chunk tokens
+// each (the very last one up to L) and start at a multiple of 32; the others
+// share the tokens before them evenly in whole 32-token tiles, so no split
+// exceeds 1.25 chunk. The queue hands out every sequence's large splits
+// before any short one, so the items taken last are short and workgroups
+// finish close together. The ranges depend on L and the plan only, never on
+// which workgroup runs them or when.
+struct SplitGeometry {
+  int nsplit;       // splits of the sequence
+  int small;        // short last splits among them
+  int small_start;  // first token of the short splits (L without them)
+  int big_tiles;    // 32-token tiles before small_start
+
+  __device__ SplitGeometry(int L, const AttnParams& p) {
+    nsplit = L > 0 ? 1 + (L - 1) / p.chunk : 1;
+    small = p.tail_chunk > 0 ? min(p.tail_splits, nsplit / 4) : 0;
+    small_start = small > 0 ? (L - small * p.tail_chunk) & ~31 : L;
+    big_tiles = small_start >> 5;
+  }
+  __device__ int big() const { return nsplit - small; }
+
+  // Tokens [t0, t1) of split j < nsplit.
+  __device__ void range(int j, int L, const AttnParams& p, int& t0, int& t1) const {
+    if (small == 0) {
+      t0 = j * p.chunk;
+      t1 = t0 + min(L - t0, p.chunk);
+    } else if (j < big()) {
+      const int64_t n = big();
+      t0 = 32 * static_cast<int>(j * static_cast<int64_t>(big_tiles) / n);
+      t1 = 32 * static_cast<int>((j + 1) * static_cast<int64_t>(big_tiles) / n);
+    } else {
+      const int s = j - big();
+      t0 = small_start + s * p.tail_chunk;
+      t1 = s == small - 1 ? L : t0 + p.tail_chunk;
+    }
+  }
+};
+
+// Attention of the G query heads of KV head hk of sequence b over split j of
+// nsplit_b (tokens [t_begin, t_end)), ending with this split's share of the
+// log-sum-exp merge. Called by every thread of the workgroup. seq_row is
+// seq_start[b] for the contiguous layout (unused when paged); the callers
+// load it together with ctx_lens[b], so the two loads cost one round trip
+// before the first tile is requested.
 //
 // With next_item set (work-queue form), thread 0 takes the workgroup's next
 // item from the queue once the token loop is done: issued earlier, the queue
 // atomic would sit ahead of the tile loads in the in-order memory counter.
 template <int D, Layout LAYOUT, bool FP8>
-__device__ void attend_split(const AttnParams& p, SplitSmem<D, LAYOUT>& sm, int b, int hk, int j, int L,
-                             int64_t seq_row, int* next_item) {
+__device__ void attend_split(const AttnParams& p, SplitSmem<D, LAYOUT>& sm, int b, int hk, int j, int nsplit_b,
+                             int t_begin, int t_end, int L, int64_t seq_row, int* next_item) {
   using TileT = typename TileOf<D, FP8>::type;
   constexpr int KB = D / 32;
   constexpr int NT = D / 16;
-  const int nsplit_b = L > 0 ? 1 + (L - 1) / p.chunk : 1;
-  const int t_begin = j * p.chunk;
-  const int t_end = t_begin + min(L - t_begin, p.chunk);
   const int lane = threadIdx.x & 63;
   const int w = uniform_i32(threadIdx.x >> 6);
   const int c = lane & 15, g = lane >> 4;
@@ -496,52 +534,73 @@ __global__ __launch_bounds__(kThreads, 2) void decode_mfma_kernel(const AttnPara
   int L;
   int64_t seq_row;
   load_sequence<LAYOUT>(p, b, L, seq_row);
-  const int nsplit_b = L > 0 ? 1 + (L - 1) / p.chunk : 1;
-  if (j >= nsplit_b) return;
+  const SplitGeometry geo(L, p);
+  if (j >= geo.nsplit) return;
+  int t0, t1;
+  geo.range(j, L, p, t0, t1);
   __shared__ SplitSmem<D, LAYOUT> sm;
-  attend_split<D, LAYOUT, FP8>(p, sm, b, hk, j, L, seq_row, nullptr);
+  attend_split<D, LAYOUT, FP8>(p, sm, b, hk, j, geo.nsplit, t0, t1, L, seq_row, nullptr);
 }
 
-// Persistent workgroups that take work items from a queue. Item i stands for
-// split j of KV head hk of sequence b, in the order (b, j, hk): the heads of
-// one token range are adjacent, sequences follow each other. Which workgroup
-// runs an item depends on timing, but every item computes the same values
-// and the merge order is fixed, so results do not. The queue counter and the
-// count of finished workgroups live next to the tickets and return to zero
-// when the last workgroup leaves. Faster XCDs and compute units simply take
-// more items, and ragged batches need no empty workgroups.
+// In-place prefix sum by one wave: a[i + 1] (counts of sequences 0..n-1)
+// becomes the total of the first i + 1 counts, and a[0] = 0.
+__device__ inline void wave_prefix_sum(int* a, int n, int lane) {
+  int carry = 0;
+  for (int base = 0; base < n; base += 64) {
+    const int i = base + lane;
+    int v = i < n ? a[i + 1] : 0;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      const int u = __shfl_up(v, o);
+      if (lane >= o) v += u;
+    }
+    if (i < n) a[i + 1] = carry + v;
+    carry += __shfl(v, 63);
+  }
+  if (lane == 0) a[0] = 0;
+}
+
+// Sequence b with first[b] <= index < first[b + 1] (first is a prefix sum).
+__device__ inline int find_sequence(const int* first, int n, int index) {
+  int lo = 0, hi = n - 1;
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (first[mid] <= index) lo = mid; else hi = mid - 1;
+  }
+  return lo;
+}
+
+// Persistent workgroups that take work items from a queue. The items are
+// the large splits of every sequence, in the order (b, j, hk) so that the
+// heads of one token range are adjacent and sequences follow each other,
+// then the short last splits (SplitGeometry) in the same order. Which
+// workgroup runs an item depends on timing, but every item computes the same
+// values and the merge order is fixed, so results do not. The queue counter
+// and the count of finished workgroups live next to the tickets and return
+// to zero when the last workgroup leaves. Faster XCDs and compute units
+// simply take more items, and ragged batches need no empty workgroups.
 template <int D, Layout LAYOUT, bool FP8>
 __global__ __launch_bounds__(kThreads, 2) void decode_mfma_queue_kernel(const AttnParams p, int batch) {
   __shared__ SplitSmem<D, LAYOUT> sm;
-  __shared__ int sm_first[kMaxQueueBatch + 1];  // first split index of each sequence; last = total
+  __shared__ int sm_first[kMaxQueueBatch + 1];  // prefix sums of large splits per sequence
+  __shared__ int sm_short[kMaxQueueBatch + 1];  // prefix sums of short splits per sequence
   __shared__ int sm_next;
   const int tid = threadIdx.x;
   uint32_t* queue = p.tickets + p.queue_slot;
   uint32_t* finished = queue + 1;
 
-  // Splits per sequence, then an exclusive prefix sum (one wave scans).
+  // Split counts per sequence, then prefix sums (one wave each).
   for (int b = tid; b < batch; b += kThreads) {
-    const int L = checked_len(p.ctx_lens[b], p.max_ctx, nullptr);  // reported by load_sequence
-    sm_first[b + 1] = L > 0 ? 1 + (L - 1) / p.chunk : 1;
+    const SplitGeometry geo(checked_len(p.ctx_lens[b], p.max_ctx, nullptr), p);  // reported by load_sequence
+    sm_first[b + 1] = geo.big();
+    sm_short[b + 1] = geo.small;
   }
   __syncthreads();
-  if (tid < 64) {
-    int carry = 0;
-    for (int base = 0; base < batch; base += 64) {
-      const int i = base + tid;
-      int v = i < batch ? sm_first[i + 1] : 0;
-#pragma unroll
-      for (int o = 1; o < 64; o <<= 1) {
-        const int u = __shfl_up(v, o);
-        if (tid >= o) v += u;
-      }
-      if (i < batch) sm_first[i + 1] = carry + v;
-      carry += __shfl(v, 63);
-    }
-    if (tid == 0) sm_first[0] = 0;
-  }
+  if (tid < 64) wave_prefix_sum(sm_first, batch, tid);
+  else if (tid < 128) wave_prefix_sum(sm_short, batch, tid - 64);
   __syncthreads();
-  const int total = sm_first[batch] * p.num_kv_heads;
+  const int total_big = sm_first[batch] * p.num_kv_heads;
+  const int total = total_big + sm_short[batch] * p.num_kv_heads;
   // Item blockIdx.x first; later items come from the queue, which hands out
   // gridDim.x, gridDim.x + 1, ... Without more items than workgroups the
   // queue is never touched.
@@ -549,18 +608,19 @@ __global__ __launch_bounds__(kThreads, 2) void decode_mfma_queue_kernel(const At
 
   int item = blockIdx.x;
   while (item < total) {
-    const int split_index = item / p.num_kv_heads;
-    const int hk = item - split_index * p.num_kv_heads;
-    int lo = 0, hi = batch - 1;  // sequence b with sm_first[b] <= split_index < sm_first[b + 1]
-    while (lo < hi) {
-      const int mid = (lo + hi + 1) >> 1;
-      if (sm_first[mid] <= split_index) lo = mid; else hi = mid - 1;
-    }
-    const int b = lo;
+    const bool is_big = item < total_big;
+    const int index = (is_big ? item : item - total_big) / p.num_kv_heads;
+    const int hk = (is_big ? item : item - total_big) - index * p.num_kv_heads;
+    const int b = find_sequence(is_big ? sm_first : sm_short, batch, index);
+    const int big_b = sm_first[b + 1] - sm_first[b];
+    const int j = is_big ? index - sm_first[b] : big_b + index - sm_short[b];
     int L;
     int64_t seq_row;
     load_sequence<LAYOUT>(p, b, L, seq_row);
-    attend_split<D, LAYOUT, FP8>(p, sm, b, hk, split_index - sm_first[b], L, seq_row, queued ? &sm_next : nullptr);
+    const SplitGeometry geo(L, p);
+    int t0, t1;
+    geo.range(j, L, p, t0, t1);
+    attend_split<D, LAYOUT, FP8>(p, sm, b, hk, j, geo.nsplit, t0, t1, L, seq_row, queued ? &sm_next : nullptr);
     __syncthreads();
     item = queued ? sm_next : total;
     __syncthreads();

@@ -359,6 +359,22 @@ def test_auto_plan_fits_init_workspace(batch, L):
         B.comem_decode_attn_destroy(p)
 
 
+@pytest.mark.parametrize("batch,L,chunk", [
+    (1, 32768, 1024),    # batch 1, 32k: 256 items of 1024 tokens, one per workgroup
+    (16, 65536, 1024),   # ragged batch up to 64k: 4096 items of 2048 would be 8 per workgroup
+    (64, 16384, 1024),   # paged batch up to 16k: likewise
+    (64, 65536, 2048),   # 16 items of 2048 tokens per workgroup
+    (8, 131072, 4096),   # 128k and longer: 4096-token splits
+])
+def test_auto_plan_split_sizes(batch, L, chunk):
+    """The matrix-core planner's split sizes on a 256-CU part (2 queue workgroups per CU)."""
+    p, ws = B.comem_decode_attn_init(_cfg(max_batch=batch, max_ctx_len=L), B.NO_DEVICE)
+    try:
+        assert B.comem_decode_attn_plan_splits(p, batch, L, ws) == (chunk, -(-L // chunk))
+    finally:
+        B.comem_decode_attn_destroy(p)
+
+
 def _prefill_args(plan, **kw):
     args = dict(plan=plan, q=A, q_start=A, q_lens=A, max_q_len=512, k=A, v=A, stride_token=8 * 128, stride_head=128,
                 seq_start=A, ctx_lens=A, batch=2, max_ctx_len=4096, out=A, lse=A, stream=None)

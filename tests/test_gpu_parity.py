@@ -216,6 +216,42 @@ def test_lse_optional():
     check(out, None, *da.reference(w), "bf16", "no lse")
 
 
+def _tail_lengths(B, max_len, seed):
+    """Ragged lengths with the cases of the short last splits: empty, one token,
+    fewer than 4 splits (none short), exact multiples of the split, a ragged last tile."""
+    r = np.random.default_rng(seed)
+    lens = r.integers(1, max_len + 1, size=B)
+    lens[:10] = [0, 1, 31, 1025, 3072, 3073, 4096, 4097, max_len, max_len - 1]
+    return lens.tolist()
+
+
+@pytest.mark.parametrize("base,ps", [(2, 0), (4, 16), (4, 64), (4, 2), (6, 0)])
+def test_short_last_splits(base, ps):
+    """Planned splits of 1024 tokens with 32 sequences x 8 KV heads x up to 8
+    splits: at least 4 work items per resident workgroup, so each sequence of 4
+    or more splits ends in short splits of 512 tokens that the queue hands out
+    last (two per sequence on 256 compute units). Parity, then three more calls
+    bit for bit equal."""
+    import torch
+
+    spec = small_spec(WORKLOADS[base], _tail_lengths(32, 8192, 36 + ps), seed=37 + base + ps, max_ctx_len=8192)
+    if ps:
+        spec = spec.replace(page_size=ps)
+    op = make_op(spec)
+    chunk, splits = op.splits(spec.batch, spec.max_ctx_len)
+    resident = 2 * torch.cuda.get_device_properties(0).multi_processor_count
+    assert chunk == 1024 and spec.batch * spec.num_kv_heads * splits >= 4 * resident
+    w = generate(spec, spare_pages=2) if ps else generate(spec)
+    dw = DeviceWorkload(w)
+    say(f"case short last splits {spec.dtype} {spec.layout} ps={ps} lens={w.ctx_lens.tolist()[:10]}")
+    first = run(dw, op)
+    ro, rl = da.reference(w)
+    check(*first, ro, rl, spec.dtype, f"short last splits {spec.layout} ps={ps}")
+    for _ in range(3):
+        again = run(dw, op)
+        assert np.array_equal(first[0], again[0]) and np.array_equal(first[1], again[1])
+
+
 @pytest.mark.parametrize("variant", ["mfma", "mfma_grid", "valu"])
 def test_split_merge_stress(variant):
     """Up to 256 splits per (sequence, KV head) and 16k workgroups: every split's
