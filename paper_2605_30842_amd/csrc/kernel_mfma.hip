@@ -342,12 +342,13 @@ struct SplitSmem {
   int32_t pages[LAYOUT == Layout::kContig ? 1 : kMaxSplitPages];
 };
 
-// The splits of a sequence of L tokens. There are ceil(L / chunk) of them
-// (one, empty, when L = 0), normally split j = tokens [j * chunk, min((j + 1)
-// * chunk, L)). With short last splits (tail_chunk > 0: work-queue form),
-// the last `small` splits, at most a quarter of them, cover tail_chunk tokens
-// each (the very last one up to L) and start at a multiple of 32; the others
-// share the tokens before them evenly in whole 32-token tiles, so no split
+// The splits of a sequence of L tokens in the work-queue form. There are
+// ceil(L / chunk) of them (one, empty, when L = 0), normally split j = tokens
+// [j * chunk, min((j + 1) * chunk, L)), as in the grid form. With short last
+// splits (tail_chunk > 0), the last `small` splits, at most a quarter of
+// them, cover tail_chunk tokens each (the very last one up to L) and start
+// at a multiple of 32; the others share the tokens before them evenly in
+// whole 32-token tiles (the first `rem` of them one tile more), so no split
 // exceeds 1.25 chunk. The queue hands out every sequence's large splits
 // before any short one, so the items taken last are short and workgroups
 // finish close together. The ranges depend on L and the plan only, never on
@@ -356,13 +357,15 @@ struct SplitGeometry {
   int nsplit;       // splits of the sequence
   int small;        // short last splits among them
   int small_start;  // first token of the short splits (L without them)
-  int big_tiles;    // 32-token tiles before small_start
+  int q, rem;       // large split j has q tiles, one more if j < rem
 
   __device__ SplitGeometry(int L, const AttnParams& p) {
     nsplit = L > 0 ? 1 + (L - 1) / p.chunk : 1;
     small = p.tail_chunk > 0 ? min(p.tail_splits, nsplit / 4) : 0;
     small_start = small > 0 ? (L - small * p.tail_chunk) & ~31 : L;
-    big_tiles = small_start >> 5;
+    const int tiles = small_start >> 5;
+    q = small > 0 ? tiles / (nsplit - small) : 0;
+    rem = small > 0 ? tiles - q * (nsplit - small) : 0;
   }
   __device__ int big() const { return nsplit - small; }
 
@@ -372,9 +375,8 @@ struct SplitGeometry {
       t0 = j * p.chunk;
       t1 = t0 + min(L - t0, p.chunk);
     } else if (j < big()) {
-      const int64_t n = big();
-      t0 = 32 * static_cast<int>(j * static_cast<int64_t>(big_tiles) / n);
-      t1 = 32 * static_cast<int>((j + 1) * static_cast<int64_t>(big_tiles) / n);
+      t0 = 32 * (j * q + min(j, rem));
+      t1 = t0 + 32 * (q + (j < rem ? 1 : 0));
     } else {
       const int s = j - big();
       t0 = small_start + s * p.tail_chunk;
@@ -534,12 +536,11 @@ __global__ __launch_bounds__(kThreads, 2) void decode_mfma_kernel(const AttnPara
   int L;
   int64_t seq_row;
   load_sequence<LAYOUT>(p, b, L, seq_row);
-  const SplitGeometry geo(L, p);
-  if (j >= geo.nsplit) return;
-  int t0, t1;
-  geo.range(j, L, p, t0, t1);
+  const int nsplit_b = L > 0 ? 1 + (L - 1) / p.chunk : 1;  // even splits (no short last ones)
+  if (j >= nsplit_b) return;
+  const int t0 = j * p.chunk;
   __shared__ SplitSmem<D, LAYOUT> sm;
-  attend_split<D, LAYOUT, FP8>(p, sm, b, hk, j, geo.nsplit, t0, t1, L, seq_row, nullptr);
+  attend_split<D, LAYOUT, FP8>(p, sm, b, hk, j, nsplit_b, t0, t0 + min(L - t0, p.chunk), L, seq_row, nullptr);
 }
 
 // In-place prefix sum by one wave: a[i + 1] (counts of sequences 0..n-1)
