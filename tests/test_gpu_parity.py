@@ -252,6 +252,52 @@ def test_short_last_splits(base, ps):
         assert np.array_equal(first[0], again[0]) and np.array_equal(first[1], again[1])
 
 
+@pytest.mark.parametrize("base,ps", [(2, 0), (4, 16), (4, 2)])
+def test_short_last_splits_fused_append(base, ps):
+    """The fused append under short last splits: the split that ends at L is a
+    short one. One launch (store, then attend) leaves the same cache bits and
+    output bits as the append call followed by the attention call."""
+    import torch
+    from workloads.synth import draw_new_rows
+    from tests.gpu_util import to_torch
+
+    spec = small_spec(WORKLOADS[base], _tail_lengths(32, 8191, 46 + ps), seed=47 + ps, max_ctx_len=8192)
+    if ps:
+        spec = spec.replace(page_size=ps)
+    w = generate(spec, spare_pages=2) if ps else generate(spec)
+    nk, nv = draw_new_rows(spec, seed=48 + ps)
+    tk, tv = to_torch(nk, spec.dtype, "cuda:0"), to_torch(nv, spec.dtype, "cuda:0")
+    a, b = DeviceWorkload(w), DeviceWorkload(w)
+    op = make_op(spec)
+    assert op.splits(spec.batch, spec.max_ctx_len)[0] == 1024
+    say(f"case short last splits, fused append {spec.layout} ps={ps}")
+    lse_a, lse_b = (torch.empty((spec.batch, spec.num_q_heads), dtype=torch.float32, device="cuda:0")
+                    for _ in range(2))
+    if ps:
+        op.append_paged(tk, tv, a.k, a.v, a.block_table, a.ctx_lens, spec.max_ctx_len)
+        out_a, _ = op.forward_paged(a.q, a.k, a.v, a.block_table, a.ctx_lens, spec.max_ctx_len, lse=lse_a)
+        out_b, _ = op.append_forward_paged(b.q, tk, tv, b.k, b.v, b.block_table, b.ctx_lens, spec.max_ctx_len,
+                                           lse=lse_b)
+    else:
+        op.append(tk, tv, a.k, a.v, a.seq_start, a.ctx_lens, spec.max_ctx_len)
+        out_a, _ = op.forward(a.q, a.k, a.v, a.seq_start, a.ctx_lens, spec.max_ctx_len, lse=lse_a)
+        out_b, _ = op.append_forward(b.q, tk, tv, b.k, b.v, b.seq_start, b.ctx_lens, spec.max_ctx_len, lse=lse_b)
+    torch.cuda.synchronize()
+    assert torch.equal(a.k, b.k) and torch.equal(a.v, b.v)
+    assert torch.equal(out_a, out_b) and torch.equal(lse_a, lse_b)
+    if ps:
+        w.k_pages = da.append_paged(w.k_pages, w.block_table, w.ctx_lens, nk)
+        w.v_pages = da.append_paged(w.v_pages, w.block_table, w.ctx_lens, nv)
+        got_k = b.k.view(torch.int16).cpu().numpy().view(np.uint16)
+        assert np.array_equal(got_k, w.k_pages)
+    else:
+        w.k = da.append_contiguous(w.k, w.seq_start, w.ctx_lens, nk)
+        w.v = da.append_contiguous(w.v, w.seq_start, w.ctx_lens, nv)
+        assert np.array_equal(b.k.view(torch.int16).cpu().numpy().view(np.uint16), w.k)
+    ro, rl = da.reference(w)
+    check(out_b.cpu().numpy(), lse_b.cpu().numpy(), ro, rl, spec.dtype, f"fused append, short splits ps={ps}")
+
+
 @pytest.mark.parametrize("variant", ["mfma", "mfma_grid", "valu"])
 def test_split_merge_stress(variant):
     """Up to 256 splits per (sequence, KV head) and 16k workgroups: every split's
