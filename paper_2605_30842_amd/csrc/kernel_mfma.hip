@@ -1,6 +1,8 @@
 // Matrix-core (MFMA) decode-attention kernel for bf16 caches on gfx950.
 //
-// One workgroup = one (split j, KV head hk, sequence b); its 4 waves take
+// One work item = one (split j, KV head hk, sequence b), run by one
+// workgroup: in the grid form one workgroup per item, in the work-queue form
+// persistent workgroups that take items from a queue. The 4 waves take
 // 32-token tiles of the split in turn. Per tile a wave computes
 //   S^T[token, head] = K_tile . Q^T    with v_mfma_f32_16x16x32_bf16
 // (16 tokens x 16 head columns per instruction; the G real heads of the GQA
