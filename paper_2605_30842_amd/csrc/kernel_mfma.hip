@@ -237,7 +237,7 @@ struct Loader {
 };
 
 template <int D>
-__device__ inline void compute_tile(const Tile<D>& T, int t0, int t_end, int c, int g,
+__device__ inline void compute_tile(const Tile<D>& T, int t0, int t_end, int g,
                                     const bf16x8 (&qop)[D / 32], float scale_log2, float& m_run,
                                     float& l_run, f32x4 (&acc)[D / 16]) {
   constexpr int KB = D / 32;
@@ -312,15 +312,15 @@ __device__ inline void compute_tile(const Tile<D>& T, int t0, int t_end, int c, 
 
 // compute_tile on a tile as loaded (FP8 tiles are widened first).
 template <int D, bool FP8>
-__device__ inline void compute_loaded(const typename TileOf<D, FP8>::type& T, int t0, int t_end, int c, int g,
+__device__ inline void compute_loaded(const typename TileOf<D, FP8>::type& T, int t0, int t_end, int g,
                                       const bf16x8 (&qop)[D / 32], float scale_log2, float& m_run, float& l_run,
                                       f32x4 (&acc)[D / 16]) {
   if constexpr (FP8) {
     Tile<D> W;
     widen_tile<D>(T, W);
-    compute_tile<D>(W, t0, t_end, c, g, qop, scale_log2, m_run, l_run, acc);
+    compute_tile<D>(W, t0, t_end, g, qop, scale_log2, m_run, l_run, acc);
   } else {
-    compute_tile<D>(T, t0, t_end, c, g, qop, scale_log2, m_run, l_run, acc);
+    compute_tile<D>(T, t0, t_end, g, qop, scale_log2, m_run, l_run, acc);
   }
 }
 
@@ -480,13 +480,13 @@ __device__ void attend_split(const AttnParams& p, SplitSmem<D, LAYOUT>& sm, int 
         int nx = ti + kWaves;
         ld.load_full(B, t_begin + 32 * (nx < nfull ? nx : ti), nx >= nfull);
         __builtin_amdgcn_sched_barrier(0);
-        compute_loaded<D, FP8>(A, t_begin + 32 * ti, t_end, c, g, qop, p.scale_log2, m_run, l_run, acc);
+        compute_loaded<D, FP8>(A, t_begin + 32 * ti, t_end, g, qop, p.scale_log2, m_run, l_run, acc);
         if (nx >= nfull) break;
         ti = nx;
         nx = ti + kWaves;
         ld.load_full(A, t_begin + 32 * (nx < nfull ? nx : ti), nx >= nfull);
         __builtin_amdgcn_sched_barrier(0);
-        compute_loaded<D, FP8>(B, t_begin + 32 * ti, t_end, c, g, qop, p.scale_log2, m_run, l_run, acc);
+        compute_loaded<D, FP8>(B, t_begin + 32 * ti, t_end, g, qop, p.scale_log2, m_run, l_run, acc);
         if (nx >= nfull) break;
         ti = nx;
       }
@@ -495,13 +495,13 @@ __device__ void attend_split(const AttnParams& p, SplitSmem<D, LAYOUT>& sm, int 
     if (ti < ntiles && (ti % kWaves) == w) {
       TileT A;
       ld.load_any(A, t_begin + 32 * ti);
-      compute_loaded<D, FP8>(A, t_begin + 32 * ti, t_end, c, g, qop, p.scale_log2, m_run, l_run, acc);
+      compute_loaded<D, FP8>(A, t_begin + 32 * ti, t_end, g, qop, p.scale_log2, m_run, l_run, acc);
     }
   } else {
     for (; ti < ntiles; ti += kWaves) {
       TileT A;
       ld.load_any(A, t_begin + 32 * ti);
-      compute_loaded<D, FP8>(A, t_begin + 32 * ti, t_end, c, g, qop, p.scale_log2, m_run, l_run, acc);
+      compute_loaded<D, FP8>(A, t_begin + 32 * ti, t_end, g, qop, p.scale_log2, m_run, l_run, acc);
     }
   }
 
