@@ -56,7 +56,10 @@ extern "C" {
  *              q_lens[b] - 1.
  *   q_start    device int64 [batch].
  *   q_lens     device int32 [batch]: M_b.
- *   max_q_len  host bound >= every q_lens[b], 0 .. max_ctx_len (0 enqueues nothing).
+ *   max_q_len  host bound >= every q_lens[b], 0 .. max_ctx_len. A call with
+ *              max_q_len = 0 or batch = 0 enqueues nothing and, once batch,
+ *              max_ctx_len and max_q_len are in range, returns COMEM_OK
+ *              without looking at any pointer (empty buffers may be NULL).
  *   k, v, stride_token, stride_head, seq_start, ctx_lens, batch, max_ctx_len:
  *              as in comem_decode_attn (ctx_lens[b] = L_b counts the new tokens).
  *   out        device float32 [total_q, h_q, d_h], 16-byte aligned.

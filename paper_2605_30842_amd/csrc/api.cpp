@@ -415,16 +415,23 @@ comem_status decode_paged(const comem_decode_attn_plan* plan, const void* q, con
   return launch(*p, true, a, batch, splits, queue, hip_stream);
 }
 
+// A prefill call with no sequence or no new token reads and writes nothing,
+// so, as for batch = 0 in the decode calls, it needs no buffers.
+bool prefill_is_empty(int32_t batch, int32_t max_q_len) { return batch == 0 || max_q_len == 0; }
+
 // Checks of a prefill call shared by both layouts; fills the kernel arguments.
 comem_status prepare_prefill(const comem_decode_attn_plan& p, const void* q, const int64_t* q_start,
                              const int32_t* q_lens, int32_t max_q_len, const void* k, const void* v,
                              int64_t stride_token, int64_t stride_head, const int32_t* ctx_lens, int32_t batch,
                              int64_t max_ctx_len, float* out, float* lse, comem::PrefillParams& a) {
   if (p.cfg.dtype != COMEM_BF16) return COMEM_ERR_UNSUPPORTED;
-  comem_status st = validate_common(p, q, k, v, stride_token, stride_head, ctx_lens, batch, max_ctx_len, out, lse,
-                                    nullptr);
-  if (st != COMEM_OK || batch == 0) return st;
+  if (batch < 0 || batch > p.cfg.max_batch) return COMEM_ERR_INVALID_SHAPE;
+  if (max_ctx_len < 0 || max_ctx_len > p.cfg.max_ctx_len) return COMEM_ERR_INVALID_SHAPE;
   if (max_q_len < 0 || max_q_len > max_ctx_len) return COMEM_ERR_INVALID_SHAPE;
+  if (prefill_is_empty(batch, max_q_len)) return COMEM_OK;
+  const comem_status st = validate_common(p, q, k, v, stride_token, stride_head, ctx_lens, batch, max_ctx_len, out,
+                                          lse, nullptr);
+  if (st != COMEM_OK) return st;
   if (q_start == nullptr || q_lens == nullptr) return COMEM_ERR_NULL_POINTER;
   if (!aligned(q_start, 8) || !aligned(q_lens, 4)) return COMEM_ERR_MISALIGNED;
   const int64_t e = elem_bytes(p.cfg);
@@ -630,10 +637,9 @@ comem_status comem_prefill_attn(const comem_decode_attn_plan* plan, const void* 
   comem::PrefillParams a;
   comem_status st = prepare_prefill(*p, q, q_start, q_lens, max_q_len, k, v, stride_token, stride_head, ctx_lens,
                                     batch, max_ctx_len, out, lse, a);
-  if (st != COMEM_OK || batch == 0) return st;
+  if (st != COMEM_OK || prefill_is_empty(batch, max_q_len)) return st;
   if (seq_start == nullptr) return COMEM_ERR_NULL_POINTER;
   if (!aligned(seq_start, 8)) return COMEM_ERR_MISALIGNED;
-  if (max_q_len == 0) return COMEM_OK;
   if (p->device == COMEM_NO_DEVICE) return COMEM_ERR_NO_DEVICE;
   a.seq_start = seq_start;
   return launch_prefill(*p, a, false, batch, max_q_len, hip_stream);
@@ -651,10 +657,9 @@ comem_status comem_prefill_attn_paged(const comem_decode_attn_plan* plan, const 
   comem::PrefillParams a;
   comem_status st = prepare_prefill(*p, q, q_start, q_lens, max_q_len, k_pages, v_pages, stride_token, stride_head,
                                     ctx_lens, batch, max_ctx_len, out, lse, a);
-  if (st != COMEM_OK || batch == 0) return st;
+  if (st != COMEM_OK || prefill_is_empty(batch, max_q_len)) return st;
   st = validate_paged(*p, stride_page, page_size, num_pages, block_table, max_pages_per_seq, max_ctx_len);
   if (st != COMEM_OK) return st;
-  if (max_q_len == 0) return COMEM_OK;
   if (p->device == COMEM_NO_DEVICE) return COMEM_ERR_NO_DEVICE;
   a.block_table = block_table;
   a.stride_page = stride_page * elem_bytes(p->cfg);

@@ -386,6 +386,11 @@ def _prefill_args(plan, **kw):
     (dict(), B.ERR_NO_DEVICE),
     (dict(batch=0, q=None), B.OK),
     (dict(max_q_len=0), B.OK),
+    # no new token anywhere: nothing to read or write, so empty buffers may be NULL
+    (dict(max_q_len=0, q=None, q_start=None, q_lens=None, k=None, v=None, seq_start=None, ctx_lens=None,
+          out=None, lse=None), B.OK),
+    (dict(max_q_len=0, batch=5), B.ERR_INVALID_SHAPE),
+    (dict(max_q_len=0, max_ctx_len=4097), B.ERR_INVALID_SHAPE),
     (dict(batch=-1), B.ERR_INVALID_SHAPE),
     (dict(batch=5), B.ERR_INVALID_SHAPE),
     (dict(max_ctx_len=4097), B.ERR_INVALID_SHAPE),
@@ -421,6 +426,7 @@ def test_prefill_validation(plan, kw, status):
     (dict(block_table=A + 2), B.ERR_MISALIGNED),
     (dict(q_lens=None), B.ERR_NULL_POINTER),
     (dict(batch=0, block_table=None), B.OK),
+    (dict(max_q_len=0, q=None, out=None, block_table=None, page_size=0), B.OK),
 ])
 def test_prefill_paged_validation(plan, kw, status):
     p, _ = plan

@@ -73,3 +73,45 @@ def test_random_case_matches_the_oracle(i):
     empty = w.ctx_lens == 0
     assert np.all(out[empty] == 0) and np.all(lse[empty] == -np.inf)
     check(out, lse, ro, rl, c["dtype"], f"random case {i}")
+
+
+NUM_PREFILL_CASES = 64
+
+
+def draw_prefill_case(i: int) -> dict:
+    r = np.random.default_rng([2027, i])
+    paged = bool(i % 2)
+    nseq = int(r.integers(1, 5))
+    lens = r.integers(1, 1201, nseq)
+    lens[r.random(nseq) < 0.2] = r.integers(1, 40)
+    new = np.minimum(lens, r.integers(1, 161, nseq))
+    uncached = (r.random(nseq) < 0.3) & (lens <= 160)
+    new[uncached] = lens[uncached]
+    new[r.random(nseq) < 0.1] = 0
+    return dict(paged=paged, hkv=int(r.integers(1, 4)), g=int(r.choice([1, 2, 4, 8, 16])),
+                d=int(r.choice([64, 128])), lens=lens.tolist(), new=new.tolist(),
+                max_ctx=int(lens.max() + r.integers(0, 100)), ps=int(1 << r.integers(0, 8)) if paged else 0,
+                seed=int(r.integers(1 << 20)), poison=bool(r.integers(2)))
+
+
+@pytest.mark.parametrize("i", range(NUM_PREFILL_CASES))
+def test_random_prefill_case_matches_the_oracle(i):
+    import oracle.prefill_attention as pa
+    from tests.gpu_util import DevicePrefill, abs_values, check_prefill, run_prefill
+    from workloads.synth import PREFILL_WORKLOADS, generate_prefill, small_prefill_spec
+
+    c = draw_prefill_case(i)
+    spec = small_prefill_spec(PREFILL_WORKLOADS[3 if c["paged"] else 1], c["lens"], c["new"], seed=c["seed"],
+                              max_ctx_len=c["max_ctx"])
+    kv = spec.kv.replace(num_q_heads=c["hkv"] * c["g"], num_kv_heads=c["hkv"], head_dim=c["d"])
+    if c["paged"]:
+        kv = kv.replace(page_size=c["ps"])
+    spec = spec.__class__(spec.name, kv, spec.new_tokens, spec.seed)
+    gen = dict(spare_pages=2, poison=c["poison"]) if c["paged"] else dict(gap_rows=3 if c["poison"] else 0,
+                                                                          poison=c["poison"])
+    pw = generate_prefill(spec, **gen)
+    say(f"random prefill case {i}: {c}")
+    out, lse = run_prefill(DevicePrefill(pw), make_op(pw.kv.spec))
+    ro, rl = pa.reference(pw)
+    ra, _ = pa.reference(abs_values(pw))
+    check_prefill(out, lse, ro, rl, ra, f"random prefill case {i}")
