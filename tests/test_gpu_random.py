@@ -5,8 +5,10 @@ enumerate: cache dtype x kernel variant x layout and page size x GQA group x
 head size x split size x ragged lengths with empty sequences, spare pool
 pages and NaN poison outside the contexts. Each draw is one test case,
 checked element by element against the oracle with the same gates as the
-other parity tests; the sizes keep the whole sweep under a minute
-on one GPU.
+other parity tests: decode attention, decode with the fused append (cache
+bits against the oracle's append, output bits against the separate calls)
+and prefill over a cached prefix. The sizes keep the whole sweep under a
+minute on one GPU.
 """
 
 import numpy as np
@@ -115,3 +117,47 @@ def test_random_prefill_case_matches_the_oracle(i):
     ro, rl = pa.reference(pw)
     ra, _ = pa.reference(abs_values(pw))
     check_prefill(out, lse, ro, rl, ra, f"random prefill case {i}")
+
+
+NUM_APPEND_CASES = 48
+
+
+@pytest.mark.parametrize("i", range(NUM_APPEND_CASES))
+def test_random_fused_append_case(i):
+    """A decode step with its new token: the fused call leaves the oracle's appended cache bit for bit and
+    gives the same output bits as the append call followed by the attention call."""
+    import torch
+
+    from tests.test_gpu_append import _append, _bitwise, _host, _oracle_append
+    from tests.gpu_util import to_torch
+    from workloads.synth import draw_new_rows
+
+    c = draw_case(10_000 + i)
+    spec, w = make_workload(c)
+    new_k, new_v = draw_new_rows(spec, seed=c["seed"] + 1)
+    say(f"random fused append case {i}: {c}")
+    op = make_op(spec, chunk=c["chunk"], variant=c["variant"])
+    nk, nv = to_torch(new_k, spec.dtype, "cuda:0"), to_torch(new_v, spec.dtype, "cuda:0")
+    fused = DeviceWorkload(w)
+    lse = torch.empty((spec.batch, spec.num_q_heads), dtype=torch.float32, device="cuda:0")
+    if c["paged"]:
+        out, lse = op.append_forward_paged(fused.q, nk, nv, fused.k, fused.v, fused.block_table, fused.ctx_lens,
+                                           spec.max_ctx_len, lse=lse)
+    else:
+        out, lse = op.append_forward(fused.q, nk, nv, fused.k, fused.v, fused.seq_start, fused.ctx_lens,
+                                     spec.max_ctx_len, lse=lse)
+    torch.cuda.synchronize()
+    want_k, want_v = _oracle_append(w, new_k, new_v)
+    _bitwise(_host(fused.k, spec.dtype), want_k, f"case {i} K cache")
+    _bitwise(_host(fused.v, spec.dtype), want_v, f"case {i} V cache")
+    sep = DeviceWorkload(w)
+    _append(sep, op, new_k, new_v)
+    out2, lse2 = run(sep, op)
+    _bitwise(out.cpu().numpy(), out2, f"case {i} out fused vs separate")
+    _bitwise(lse.cpu().numpy(), lse2, f"case {i} lse fused vs separate")
+    if c["paged"]:
+        w.k_pages, w.v_pages = want_k, want_v
+    else:
+        w.k, w.v = want_k, want_v
+    ro, rl = da.reference(w)
+    check(out.cpu().numpy(), lse.cpu().numpy(), ro, rl, spec.dtype, f"random fused append case {i}")
