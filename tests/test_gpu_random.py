@@ -161,3 +161,52 @@ def test_random_fused_append_case(i):
         w.k, w.v = want_k, want_v
     ro, rl = da.reference(w)
     check(out.cpu().numpy(), lse.cpu().numpy(), ro, rl, spec.dtype, f"random fused append case {i}")
+
+
+NUM_QUEUE_CASES = 12
+
+
+def draw_queue_case(i: int) -> dict:
+    """Batches large enough for the work queue's short last splits: 8 KV heads, up to 16K tokens, planned
+    splits (at least 4 items per resident workgroup on 256 compute units)."""
+    r = np.random.default_rng([2028, i])
+    dtype = ["bf16", "fp8"][i % 2]
+    paged = bool((i // 2) % 2)
+    nseq = int(r.integers(16, 41))
+    lens = r.integers(0, 16385, nseq)
+    lens[r.random(nseq) < 0.1] = 0
+    lens[0] = 16384
+    return dict(dtype=dtype, paged=paged, variant=str(r.choice(["auto", "mfma"])), hkv=8,
+                g=int(r.choice([4, 8])), d=128, lens=lens.tolist(), max_ctx=16384,
+                ps=int(r.choice([2, 16, 64, 128])) if paged else 0, chunk=0, seed=int(r.integers(1 << 20)),
+                poison=bool(r.integers(2)))
+
+
+@pytest.mark.parametrize("i", range(NUM_QUEUE_CASES))
+def test_random_queue_case_matches_the_oracle(i):
+    import torch
+
+    c = draw_queue_case(i)
+    spec, w = make_workload(c)
+    op = make_op(spec, chunk=0, variant=c["variant"])
+    chunk, splits = op.splits(spec.batch, spec.max_ctx_len)
+    resident = 2 * torch.cuda.get_device_properties(0).multi_processor_count
+    assert chunk == 1024 and spec.batch * spec.num_kv_heads * splits >= 4 * resident
+    say(f"random queue case {i}: {dict(c, lens=c['lens'][:6])}")
+    out, lse = run(DeviceWorkload(w), op)
+    if c["dtype"] == "bf16":
+        ro, rl = da.reference(w)
+        check(out, lse, ro, rl, c["dtype"], f"random queue case {i}")
+        return
+    # FP8: sampled rows of six sequences, the longest among them (the oracle widens a sequence's every code)
+    r = np.random.default_rng([2029, i])
+    hq = spec.num_q_heads
+    seqs = {0, *(int(b) for b in r.choice(spec.batch, size=5, replace=False))}
+    rows = sorted({*((b, 0) for b in seqs), *((b, hq - 1) for b in seqs),
+                   *((b, int(r.integers(hq))) for b in seqs for _ in range(3))})
+    ref = da.decode_attention_rows(w, rows)
+    check(np.stack([out[b, h] for b, h in rows]), np.array([lse[b, h] for b, h in rows]),
+          np.stack([o for o, _ in ref]), np.array([l for _, l in ref]), c["dtype"], f"random queue case {i}")
+    empty = w.ctx_lens == 0
+    assert np.all(out[empty] == 0) and np.all(lse[empty] == -np.inf)
+    assert np.all(np.isfinite(out)) and np.all(np.isfinite(lse[~empty]))
