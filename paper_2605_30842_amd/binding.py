@@ -78,6 +78,21 @@ class ComemError(RuntimeError):
 _lib = None
 
 
+def _hip_runtime_first() -> None:
+    """Load torch (and with it the HIP runtime it ships) before the library.
+
+    The library links the system HIP runtime; torch ships its own. The
+    dynamic linker keeps whichever loads first, so opening the library before
+    importing torch would put torch on the library's runtime. With torch
+    first, both use torch's, the arrangement every test and measurement here
+    runs in.
+    """
+    try:
+        import torch  # noqa: F401
+    except ImportError:
+        pass
+
+
 def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     """Load the built library once; raise if it has not been built."""
     global _lib
@@ -85,6 +100,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         return _lib
     if not os.path.exists(path):
         raise RuntimeError(f"{path} not found: build it with `python -m paper_2605_30842_amd.build`")
+    _hip_runtime_first()
     lib = ctypes.CDLL(path)
     vp, i32, i64, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t
     lib.comem_decode_attn_init.argtypes = [ctypes.POINTER(Config), ctypes.c_int, ctypes.POINTER(vp),
@@ -140,6 +156,7 @@ def load_probe_library(path: str = PROBE_LIB_PATH) -> ctypes.CDLL:
         return _probe
     if not os.path.exists(path):
         raise RuntimeError(f"{path} not found: build it with `python -m paper_2605_30842_amd.build`")
+    _hip_runtime_first()
     lib = ctypes.CDLL(path)
     vp, sz = ctypes.c_void_p, ctypes.c_size_t
     lib.comem_probe_read.argtypes = [vp, sz, vp, ctypes.c_int, vp]

@@ -127,15 +127,20 @@ def test_valid_calls_at_the_plan_limits_pass_validation(cfg, log_ps):
         assert lib.comem_decode_attn_destroy(plan) == B.OK
 
 
+_PLAN = []
+
+
 def _plan():
-    cfg = B.Config(num_q_heads=32, num_kv_heads=8, head_dim=128, dtype=B.BF16, scale=0.088, max_batch=8,
-                   max_ctx_len=8192, chunk_tokens=0, variant=B.VARIANT_AUTO, k_scale=1.0, v_scale=1.0)
-    status, plan, ws = _init(cfg)
-    assert status == B.OK
-    return plan, ws
+    """One device-less plan shared by the call tests, made on first use (not when pytest collects)."""
+    if not _PLAN:
+        cfg = B.Config(num_q_heads=32, num_kv_heads=8, head_dim=128, dtype=B.BF16, scale=0.088, max_batch=8,
+                       max_ctx_len=8192, chunk_tokens=0, variant=B.VARIANT_AUTO, k_scale=1.0, v_scale=1.0)
+        status, plan, _ = _init(cfg)
+        assert status == B.OK
+        _PLAN.append(plan)
+    return _PLAN[0]
 
 
-PLAN, WS = _plan()
 sizes = st.integers(-3, 1 << 40)
 
 
@@ -145,7 +150,7 @@ sizes = st.integers(-3, 1 << 40)
        batch=st.integers(-2, 12), max_ctx=st.integers(-2, 20000), ws_bytes=sizes)
 def test_contiguous_call_returns_a_status(q, k, v, out, lse, ws_ptr, seq, lens, stride_token, stride_head,
                                           batch, max_ctx, ws_bytes):
-    status = B.load_library().comem_decode_attn(PLAN, q, k, v, stride_token, stride_head, seq, lens, batch,
+    status = B.load_library().comem_decode_attn(_plan(), q, k, v, stride_token, stride_head, seq, lens, batch,
                                                 max_ctx, out, lse, ws_ptr, ws_bytes, None)
     assert status in STATUSES
     assert status != B.OK or batch == 0  # a device-less plan launches nothing
@@ -159,7 +164,7 @@ def test_contiguous_call_returns_a_status(q, k, v, out, lse, ws_ptr, seq, lens, 
        batch=st.integers(-2, 12), max_ctx=st.integers(-2, 20000), ws_bytes=sizes)
 def test_paged_call_returns_a_status(q, k, bt, lens, ws_ptr, stride_page, stride_token, page_size, num_pages,
                                      max_pages, batch, max_ctx, ws_bytes):
-    status = B.load_library().comem_decode_attn_paged(PLAN, q, k, k, stride_page, stride_token, 128, page_size,
+    status = B.load_library().comem_decode_attn_paged(_plan(), q, k, k, stride_page, stride_token, 128, page_size,
                                                       num_pages, bt, max_pages, lens, batch, max_ctx, A, A, ws_ptr,
                                                       ws_bytes, None)
     assert status in STATUSES
@@ -171,7 +176,7 @@ def test_paged_call_returns_a_status(q, k, bt, lens, ws_ptr, stride_page, stride
 @given(q=pointers, qs=pointers, ql=pointers, seq=pointers, lens=pointers, max_q=st.integers(-2, 1 << 20),
        stride_token=st.integers(-8, 1 << 28), batch=st.integers(-2, 12), max_ctx=st.integers(-2, 20000))
 def test_prefill_call_returns_a_status(q, qs, ql, seq, lens, max_q, stride_token, batch, max_ctx):
-    status = B.load_library().comem_prefill_attn(PLAN, q, qs, ql, max_q, A, A, stride_token, 128, seq, lens, batch,
+    status = B.load_library().comem_prefill_attn(_plan(), q, qs, ql, max_q, A, A, stride_token, 128, seq, lens, batch,
                                                  max_ctx, A, A, None)
     assert status in STATUSES
     assert status != B.OK or batch == 0 or max_q == 0
