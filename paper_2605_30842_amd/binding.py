@@ -81,11 +81,10 @@ _lib = None
 def _hip_runtime_first() -> None:
     """Load torch (and with it the HIP runtime it ships) before the library.
 
-    The library links the system HIP runtime; torch ships its own. The
-    dynamic linker keeps whichever loads first, so opening the library before
-    importing torch would put torch on the library's runtime. With torch
-    first, both use torch's, the arrangement every test and measurement here
-    runs in.
+    The library links the system HIP runtime; torch ships its own, and which
+    one the process uses depends on what loads first. With the library opened
+    first, the library's device queries failed once torch was imported; with
+    torch first, everything here runs.
     """
     try:
         import torch  # noqa: F401
