@@ -38,6 +38,23 @@ def test_full_workload_every_output(i):
     say(f"  max |err| {err:.3e}")
 
 
+def test_headline_workload_repeated_calls_bitwise():
+    """The batch-1 32K workload's 32 splits per KV head finish in an order
+    that changes from call to call, so a different workgroup merges each
+    head from call to call. Every call must give the same bits (the merge
+    visits splits in index order), and the first must pass the gate."""
+    w = generate(WORKLOADS[2])
+    say(f"case repeated calls {w.spec.name}")
+    dw = DeviceWorkload(w)
+    op = make_op(w.spec)
+    first = run(dw, op)
+    ro, rl = da.reference(w)
+    check(*first, ro, rl, w.spec.dtype, w.spec.name)
+    for k in range(24):
+        again = run(dw, op)
+        assert np.array_equal(first[0], again[0]) and np.array_equal(first[1], again[1]), f"call {k + 1}"
+
+
 @pytest.mark.parametrize("i", [3, 4, 5])
 def test_full_workload_sampled_rows(i):
     import torch
