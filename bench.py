@@ -57,6 +57,9 @@ def _args():
                          "step: the append call then the attention call; fused: both in one launch")
     ap.add_argument("--variant", default="auto", choices=["auto", "mfma", "mfma_grid", "valu"])
     ap.add_argument("--chunk", type=int, default=0, help="tokens per split (0 = planned)")
+    ap.add_argument("--kv-placement", default="offset", choices=["offset", "separate"],
+                    help="offset: K and V of each copy in one allocation, V's base 256 bytes past K's modulo 512 "
+                         "(the placement the C header recommends); separate: two allocations (bases equal modulo 4096)")
     ap.add_argument("--copies", type=int, default=0, help="KV copies to cycle over (0 = enough to exceed the LLC)")
     ap.add_argument("--cpu-seconds", type=float, default=10.0, help="budget of the CPU oracle baseline (0 = skip)")
     ap.add_argument("--timing", default="graph", choices=["graph", "eager"],
@@ -533,7 +536,17 @@ def main():
     paged = spec.layout == "paged"
     k0 = dev_t(w.k_pages if paged else w.k)
     v0 = dev_t(w.v_pages if paged else w.v)
-    kv = [(k0, v0)] + [(k0.clone(), v0.clone()) for _ in range(copies - 1)]
+    if a.kv_placement == "offset":
+        kv = []
+        for _ in range(copies):
+            kc, vc = binding.kv_cache_pair(tuple(k0.shape), k0.dtype, dev)
+            kc.copy_(k0)
+            vc.copy_(v0)
+            kv.append((kc, vc))
+        del k0, v0
+    else:
+        kv = [(k0, v0)] + [(k0.clone(), v0.clone()) for _ in range(copies - 1)]
+    v_minus_k = sorted({(int(vc.data_ptr()) - int(kc.data_ptr())) % 4096 for kc, vc in kv})
     if paged:
         bt = torch.from_numpy(w.block_table.astype(np.int32)).to(dev)
     else:
@@ -664,7 +677,8 @@ def main():
             "workload": spec.name, "batch": spec.batch, "num_q_heads": spec.num_q_heads,
             "num_kv_heads": spec.num_kv_heads, "head_dim": spec.head_dim, "ctx_len_total": int(w.ctx_lens.sum()),
             "layout": spec.layout, "page_size": spec.page_size, "kv_bytes_per_step": kv_bytes,
-            "kv_copies_cycled": copies, "chunk_tokens": chunk, "splits": splits, "kernel": kind,
+            "kv_copies_cycled": copies, "kv_placement": a.kv_placement, "v_minus_k_base_mod_4096": v_minus_k,
+            "chunk_tokens": chunk, "splits": splits, "kernel": kind,
             "timing": a.timing, "eager_us_per_step": round(eager_ms * 1e3, 3), "op": a.op,
             "single_call_us": pct,
         },

@@ -318,6 +318,33 @@ def comem_cost_max_compression_ratio(inputs: CostInputs) -> float:
 # ------------------------------------------------------------ torch wrapper
 
 
+# Placement of V relative to K that the C header recommends
+# (COMEM_V_BASE_OFFSET_BYTES modulo COMEM_V_BASE_OFFSET_MODULUS).
+V_BASE_OFFSET_BYTES = 256
+V_BASE_OFFSET_MODULUS = 512
+
+
+def kv_cache_pair(shape, dtype, device):
+    """Empty K and V caches of `shape` carved from one allocation, with V's base
+    at K's base plus V_BASE_OFFSET_BYTES modulo V_BASE_OFFSET_MODULUS (whatever
+    the allocation's own alignment). Both are contiguous tensors."""
+    import math
+
+    import torch
+
+    esize = torch.empty((), dtype=dtype).element_size()
+    n = math.prod(shape)
+    nbytes = n * esize
+    gap = (V_BASE_OFFSET_BYTES - nbytes) % V_BASE_OFFSET_MODULUS  # bytes between K's end and V's start
+    assert gap % esize == 0
+    g = gap // esize
+    buf = torch.empty(2 * n + g, dtype=dtype, device=device)
+    k = buf[:n].view(shape)
+    v = buf[n + g:2 * n + g].view(shape)
+    assert (v.data_ptr() - k.data_ptr()) % V_BASE_OFFSET_MODULUS == V_BASE_OFFSET_BYTES
+    return k, v
+
+
 class DecodeAttention:
     """A plan plus its workspace, called with torch device tensors.
 

@@ -473,3 +473,24 @@ def test_fp8_strides_are_bytes():
         assert lib.comem_prefill_attn(*_prefill_args(p).values()) == B.ERR_UNSUPPORTED
     finally:
         B.comem_decode_attn_destroy(p)
+
+
+@pytest.mark.parametrize("shape", [(1,), (3, 5, 7), (33, 8, 128), (2, 16, 8, 64)])
+@pytest.mark.parametrize("dtype", ["uint8", "bfloat16", "float32"])
+def test_kv_cache_pair_places_v_256_bytes_past_k_modulo_512(shape, dtype):
+    """The helper's V base is K's plus 256 modulo 512 for any size and element
+    type (on CPU tensors; the arithmetic does not depend on the device), and
+    the two caches do not overlap."""
+    import torch
+
+    from paper_2605_30842_amd.binding import kv_cache_pair
+
+    dt = getattr(torch, dtype)
+    k, v = kv_cache_pair(shape, dt, "cpu")
+    assert k.shape == v.shape == shape and k.dtype == v.dtype == dt
+    assert k.is_contiguous() and v.is_contiguous()
+    assert (v.data_ptr() - k.data_ptr()) % 512 == 256
+    assert v.data_ptr() >= k.data_ptr() + k.numel() * k.element_size()
+    k.fill_(1)
+    v.fill_(2)
+    assert int(k.min()) == 1 and int(v.max()) == 2

@@ -313,3 +313,31 @@ def test_split_merge_stress(variant):
     for _ in range(4):
         again = run(dw, op)
         assert np.array_equal(first[0], again[0]) and np.array_equal(first[1], again[1])
+
+
+@pytest.mark.parametrize("base,lens", [(2, [4100, 777, 1, 0]), (5, [3000, 65, 1]), (6, [4100, 777, 1]),
+                                       (7, [3000, 65, 1])])
+def test_kv_placement_gives_the_same_bits(base, lens):
+    """The recommended placement (K and V in one buffer, V's base 256 bytes past
+    K's modulo 512) changes only where the rows sit: the outputs equal those of
+    two separate allocations bit for bit, and pass the gate."""
+    import torch
+
+    from paper_2605_30842_amd import binding
+
+    spec = small_spec(WORKLOADS[base], lens, seed=41 + base)
+    w = generate(spec)
+    dw = DeviceWorkload(w)
+    op = make_op(spec)
+    say(f"case kv placement workload {base} {spec.dtype} {spec.layout} lens={lens}")
+    separate = run(dw, op)
+    k, v = binding.kv_cache_pair(tuple(dw.k.shape), dw.k.dtype, dw.k.device)
+    k.copy_(dw.k)
+    v.copy_(dw.v)
+    assert (v.data_ptr() - k.data_ptr()) % 512 == 256
+    dw.k, dw.v = k, v
+    placed = run(dw, op)
+    assert np.array_equal(separate[0], placed[0]) and np.array_equal(separate[1], placed[1])
+    ro, rl = da.reference(w)
+    check(*placed, ro, rl, spec.dtype, f"placement workload {base}")
+    torch.cuda.synchronize()
