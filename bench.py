@@ -448,6 +448,12 @@ def _prefill(a):
     paged = s.layout == "paged"
     k = dev_t(pw.kv.k_pages if paged else pw.kv.k)
     v = dev_t(pw.kv.v_pages if paged else pw.kv.v)
+    if a.kv_placement == "offset":  # one allocation, V's base 256 bytes past K's modulo 512
+        kc, vc = binding.kv_cache_pair(tuple(k.shape), k.dtype, dev)
+        kc.copy_(k)
+        vc.copy_(v)
+        k, v = kc, vc
+    v_minus_k = (int(v.data_ptr()) - int(k.data_ptr())) % 4096
     bt = torch.from_numpy(pw.kv.block_table.astype(np.int32)).to(dev) if paged else None
     ss = None if paged else torch.from_numpy(pw.kv.seq_start.astype(np.int64)).to(dev)
     op = DecodeAttention(s.num_q_heads, s.num_kv_heads, s.head_dim, s.dtype, float(s.scale), s.batch,
@@ -487,7 +493,8 @@ def _prefill(a):
         "config": {"workload": pspec.name, "batch": s.batch, "num_q_heads": s.num_q_heads,
                    "num_kv_heads": s.num_kv_heads, "head_dim": s.head_dim, "layout": s.layout,
                    "page_size": s.page_size, "new_tokens": int(pw.q_lens.sum()),
-                   "cached_tokens": int(pw.kv.ctx_lens.sum()), "flops_per_step": flops, "timing": "eager"},
+                   "cached_tokens": int(pw.kv.ctx_lens.sum()), "flops_per_step": flops, "timing": "eager",
+                   "kv_placement": a.kv_placement, "v_minus_k_base_mod_4096": v_minus_k},
         "roofline": {"bound": "mfma", "achieved": round(tflops, 3), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                      "frac": round(tflops / PEAK_BF16_TFLOPS, 4),
                      "traffic": recorded_traffic(pspec.name, PREFILL_SOURCES, "algorithmic_flops")},
