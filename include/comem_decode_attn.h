@@ -171,7 +171,10 @@ comem_status comem_decode_attn_device_errors(const comem_decode_attn_plan* plan,
  * 2048 and 3072 the slower one. For paged caches the same applies to the V
  * pool's base against the K pool's. One way to get it: allocate K and V as
  * one buffer with V starting at the first address past K's end that is 256
- * bytes past K's base modulo 512. */
+ * bytes past K's base modulo 512. What counts is the address difference
+ * between the V and the K row of the same token and head: for K and V
+ * interleaved in one buffer (for example [T, 2, h_kv, d_h]) it is the offset
+ * of the V part within a token, which should then be 256 modulo 512 too. */
 #define COMEM_V_BASE_OFFSET_BYTES 256
 #define COMEM_V_BASE_OFFSET_MODULUS 512
 
