@@ -174,7 +174,10 @@ comem_status comem_decode_attn_device_errors(const comem_decode_attn_plan* plan,
  * bytes past K's base modulo 512. What counts is the address difference
  * between the V and the K row of the same token and head: for K and V
  * interleaved in one buffer (for example [T, 2, h_kv, d_h]) it is the offset
- * of the V part within a token, which should then be 256 modulo 512 too. */
+ * of the V part within a token, which should then be 256 modulo 512 too
+ * (the batch-1 32768-token step over [T, 2, 8, 128]: 31.9 us single calls
+ * with V at +2048 bytes, 29.1 us with each token row padded by 256 bytes and
+ * V at +2304). */
 #define COMEM_V_BASE_OFFSET_BYTES 256
 #define COMEM_V_BASE_OFFSET_MODULUS 512
 
