@@ -160,3 +160,25 @@ def test_named_workload_sampled_rows(n):
     for (b, i, h), (ro, rl), (ra, _) in zip(rows, got, got_abs):
         r = int(pw.q_start[b]) + i
         check_prefill(out[r, h][None], lse[r, h][None], ro[None], np.array([rl]), ra[None], f"row {(b, i, h)}")
+
+
+@pytest.mark.parametrize("base", [1, 3])
+def test_kv_placement_gives_the_same_bits(base):
+    """K and V carved from one allocation with V's base 256 bytes past K's
+    modulo 512 (how the bench places them) give the same bits as two separate
+    allocations, contiguous and paged."""
+    import torch
+
+    from paper_2605_30842_amd import binding
+
+    spec = small_prefill_spec(PREFILL_WORKLOADS[base], RAGGED_L, RAGGED_M, seed=57 + base)
+    pw, dp, op, out, lse, ro, rl, ra = _prefill_case(spec)
+    k, v = binding.kv_cache_pair(tuple(dp.kv.k.shape), dp.kv.k.dtype, dp.kv.k.device)
+    k.copy_(dp.kv.k)
+    v.copy_(dp.kv.v)
+    assert (v.data_ptr() - k.data_ptr()) % 512 == 256
+    dp.kv.k, dp.kv.v = k, v
+    out2, lse2 = run_prefill(dp, op)
+    assert np.array_equal(out, out2) and np.array_equal(lse, lse2)
+    check_prefill(out2, lse2, ro, rl, ra, f"placement prefill {base}")
+    torch.cuda.synchronize()
