@@ -10,7 +10,12 @@ step touched.
 
 Prints one JSON line: effective GB/s = algorithmic K+V bytes / step time,
 the roofline object for the kernel (HBM bound, 8 TB/s peak), and the CPU
-oracle timed on a bounded sample as a reported baseline.
+oracle timed on a bounded sample as a reported baseline. The same run also
+times, with the same rules, the headline workload with its K and V caches in
+the other placement, the other workloads of the 32k-128k range (batch 16
+ragged up to 64K, batch 64 paged, batch 8 at 128K), and a streaming read of
+4 GiB and of the headline's byte count (the practical read ceiling); those
+go under config.also and roofline.read_ceiling (--no-also skips them).
 """
 
 from __future__ import annotations
@@ -70,6 +75,12 @@ def _args():
     ap.add_argument("--probe-blocks", type=int, default=4096)
     ap.add_argument("--prefill", type=int, default=0,
                     help="instead of decode, time the prefill-attention call on named prefill workload N (1..3)")
+    ap.add_argument("--no-also", dest="also", action="store_false",
+                    help="time only the named workload (by default the run also times the other placement of its "
+                         "K/V caches, the other long-context workloads and the streaming-read ceiling)")
+    ap.add_argument("--also-workloads", type=lambda s: [int(x) for x in s.split(",") if x], default=[3, 4, 5],
+                    help="comma-separated workloads timed beside the headline (default 3,4,5)")
+    ap.add_argument("--also-steps", type=int, default=50, help="timed steps of each of those workloads")
     ap.add_argument("--summarize", metavar="DIR", default=None,
                     help="write profiles/ summaries from rocprofv3 outputs under DIR (layout in summarize())")
     return ap.parse_args()
@@ -242,8 +253,8 @@ def summarize(a):
             w = generate(spec)
             units = {"algorithmic_bytes": w.kv_bytes}
             sources = KERNEL_SOURCES
-            bench_args = f"--workload {i} --cpu-seconds 0"
-            pmc_args = f"--workload {i} --timing eager --steps 4 --warmup 1 --cpu-seconds 0"
+            bench_args = f"--workload {i} --cpu-seconds 0 --no-also"
+            pmc_args = f"--workload {i} --timing eager --steps 4 --warmup 1 --cpu-seconds 0 --no-also"
         else:
             pw = generate_prefill(spec)
             units = {"algorithmic_flops": pw.flops, "kv_bytes": pw.kv.kv_bytes}
@@ -502,24 +513,14 @@ def _prefill(a):
     }), flush=True)
 
 
-def main():
-    a = _args()
-    if a.gpus != 1:
-        print(f"bench.py runs on one GPU only (asked for --gpus {a.gpus}); this build has no multi-GPU path.",
-              file=sys.stderr)
-        sys.exit(2)
-    if a.steps < 1 or a.warmup < 0:
-        print("--steps must be at least 1 and --warmup at least 0", file=sys.stderr)
-        sys.exit(2)
-    if a.probe:
-        _probe(a)
-        return
-    if a.summarize:
-        summarize(a)
-        return
-    if a.prefill:
-        _prefill(a)
-        return
+def _measure_decode(a, wl, placement, steps, warmup, op_kind="attention", single_calls=True, want_w=False):
+    """Time `steps` decode steps of named workload `wl` with graph (or eager) timing; return a result dict.
+
+    Inputs are drawn on the host, copied to HBM before the timed region, and
+    (for workloads that fit the last-level cache) replicated so that every
+    step reads memory no recent step touched. Graph replays are checked bit
+    for bit against the eager result.
+    """
     import torch
 
     from paper_2605_30842_amd import binding
@@ -527,7 +528,7 @@ def main():
     from workloads.synth import WORKLOADS, draw_new_rows, generate
 
     binding.load_library()
-    spec = WORKLOADS[a.workload]
+    spec = WORKLOADS[wl]
     w = generate(spec)
     kv_bytes = w.kv_bytes
     dev = torch.device("cuda:0")
@@ -543,7 +544,7 @@ def main():
     paged = spec.layout == "paged"
     k0 = dev_t(w.k_pages if paged else w.k)
     v0 = dev_t(w.v_pages if paged else w.v)
-    if a.kv_placement == "offset":
+    if placement == "offset":
         kv = []
         for _ in range(copies):
             kc, vc = binding.kv_cache_pair(tuple(k0.shape), k0.dtype, dev)
@@ -554,10 +555,8 @@ def main():
     else:
         kv = [(k0, v0)] + [(k0.clone(), v0.clone()) for _ in range(copies - 1)]
     v_minus_k = sorted({(int(vc.data_ptr()) - int(kc.data_ptr())) % 4096 for kc, vc in kv})
-    if paged:
-        bt = torch.from_numpy(w.block_table.astype(np.int32)).to(dev)
-    else:
-        ss = torch.from_numpy(w.seq_start.astype(np.int64)).to(dev)
+    bt = torch.from_numpy(w.block_table.astype(np.int32)).to(dev) if paged else None
+    ss = None if paged else torch.from_numpy(w.seq_start.astype(np.int64)).to(dev)
     scales = dict(k_scale=spec.k_scale, v_scale=spec.v_scale) if spec.dtype == "fp8" else {}
     op = DecodeAttention(spec.num_q_heads, spec.num_kv_heads, spec.head_dim, spec.dtype, float(spec.scale),
                          spec.batch, spec.max_ctx_len, chunk_tokens=a.chunk, variant=a.variant, **scales)
@@ -565,11 +564,10 @@ def main():
     out = torch.zeros((spec.batch, spec.num_q_heads, spec.head_dim), dtype=torch.float32, device=dev)
     lse = torch.empty((spec.batch, spec.num_q_heads), dtype=torch.float32, device=dev)
     new_k, new_v = (dev_t(x) for x in draw_new_rows(spec, seed=spec.seed + 100))
-    attend = a.op != "append"
 
     def step(i, stream):
         k, v = kv[i % copies]
-        if a.op == "fused":  # the new token's rows are stored by the attention launch itself
+        if op_kind == "fused":  # the new token's rows are stored by the attention launch itself
             if paged:
                 op.append_forward_paged(q, new_k, new_v, k, v, bt, ctx, spec.max_ctx_len, out=out, lse=lse,
                                         stream=stream)
@@ -577,19 +575,19 @@ def main():
                 op.append_forward(q, new_k, new_v, k, v, ss, ctx, spec.max_ctx_len, out=out, lse=lse,
                                   stream=stream)
             return
-        if a.op != "attention":  # the new token's rows are stored first (same row on every step)
+        if op_kind != "attention":  # the new token's rows are stored first (same row on every step)
             if paged:
                 op.append_paged(new_k, new_v, k, v, bt, ctx, spec.max_ctx_len, stream=stream)
             else:
                 op.append(new_k, new_v, k, v, ss, ctx, spec.max_ctx_len, stream=stream)
-        if attend:
+        if op_kind != "append":
             if paged:
                 op.forward_paged(q, k, v, bt, ctx, spec.max_ctx_len, out=out, lse=lse, stream=stream)
             else:
                 op.forward(q, k, v, ss, ctx, spec.max_ctx_len, out=out, lse=lse, stream=stream)
 
     stream = torch.cuda.current_stream()
-    for i in range(a.warmup):
+    for i in range(warmup):
         step(i, stream)
     torch.cuda.synchronize()
     eager_out = out.clone()
@@ -604,8 +602,7 @@ def main():
         torch.cuda.synchronize()
         return e0.elapsed_time(e1) / n
 
-    eager_ms = timed(lambda: [step(i, stream) for i in range(a.steps)], a.steps)
-    steps = a.steps
+    eager_ms = timed(lambda: [step(i, stream) for i in range(steps)], steps)
     ms = eager_ms
     if a.timing == "graph":
         # One graph holds at least 16 launches, cycling over the KV copies, so
@@ -613,7 +610,7 @@ def main():
         # region replays it, and a second graph of the remaining launches
         # (the copies continue in order), so that exactly `steps` are timed.
         per_graph = copies * max(1, -(-16 // copies))
-        full, rem = divmod(a.steps, per_graph)
+        full, rem = divmod(steps, per_graph)
 
         def capture(n):
             g = torch.cuda.CUDAGraph()
@@ -632,14 +629,110 @@ def main():
                 g.replay()
                 torch.cuda.synchronize()
                 assert torch.equal(out, eager_out), "graph replay differs from eager result"
-        ms = timed(lambda: [g.replay() for g in graphs], a.steps)
+        ms = timed(lambda: [g.replay() for g in graphs], steps)
+    assert torch.isfinite(out).all().item()
+    pct = None
+    if single_calls:
+        # Spread of single calls (after the timed region): each of 100 eager
+        # calls bracketed by its own pair of events on the stream.
+        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(100)]
+        for i, (b0, b1) in enumerate(ev):
+            b0.record(stream)
+            step(i, stream)
+            b1.record(stream)
+        torch.cuda.synchronize()
+        per_call = sorted(b0.elapsed_time(b1) * 1e3 for b0, b1 in ev)
+        pct = {f"p{q}": round(per_call[min(len(per_call) - 1, q * len(per_call) // 100)], 3) for q in (10, 50, 90)}
+    res = {"spec": spec, "ms": ms, "eager_ms": eager_ms, "single_call_us": pct, "kv_bytes": kv_bytes,
+           "copies": copies, "v_minus_k": v_minus_k, "chunk": chunk, "splits": splits,
+           "ctx_len_total": int(w.ctx_lens.sum()), "w": w if want_w else None}
+    del kv, q, out, lse, op
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    return res
+
+
+def _read_ceiling(nbytes, steps, blocks=4096):
+    """Streaming read of `nbytes` (the practical HBM read ceiling), timed like the decode steps: graph replays
+    of back-to-back launches, cycling over enough buffers that each launch reads memory no recent one touched."""
+    import torch
+
+    from paper_2605_30842_amd import binding
+
+    binding.load_probe_library()
+    copies = max(1, math.ceil(4 * MALL_BYTES / nbytes))
+    bufs = [torch.ones(nbytes // 4, dtype=torch.int32, device="cuda") for _ in range(copies)]
+    sink = torch.zeros(256 * blocks, dtype=torch.int32, device="cuda")
+    stream = torch.cuda.current_stream()
+    per_graph = copies * max(1, -(-16 // copies))
+    g = torch.cuda.CUDAGraph()
+    side = torch.cuda.Stream()
+    side.wait_stream(stream)
+    with torch.cuda.graph(g, stream=side):
+        for i in range(per_graph):
+            binding.comem_probe_read(bufs[i % copies].data_ptr(), nbytes, sink.data_ptr(), blocks,
+                                     torch.cuda.current_stream().cuda_stream)
+    torch.cuda.synchronize()
+    reps = max(1, steps // per_graph)
+    g.replay()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(reps):
+        g.replay()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    us = e0.elapsed_time(e1) * 1e3 / (reps * per_graph)
+    del bufs, sink, g
+    torch.cuda.empty_cache()
+    return {"bytes": nbytes, "blocks": blocks, "us_per_call": round(us, 3),
+            "GBps": round(nbytes / (us * 1e-6) / 1e9, 1), "frac_of_peak": round(nbytes / (us * 1e-6) / 1e9 /
+                                                                               PEAK_HBM_GBPS, 4),
+            "buffers_cycled": copies}
+
+
+def _summary(r):
+    gbps = r["kv_bytes"] / (r["ms"] * 1e-3) / 1e9
+    d = {"us_per_step": round(r["ms"] * 1e3, 3), "GBps": round(gbps, 1), "frac_of_peak": round(gbps / PEAK_HBM_GBPS, 4),
+         "decode_tok_per_s": round(r["spec"].batch / (r["ms"] * 1e-3), 1), "kv_bytes_per_step": r["kv_bytes"],
+         "ctx_len_total": r["ctx_len_total"], "chunk_tokens": r["chunk"], "splits": r["splits"],
+         "kv_copies_cycled": r["copies"], "v_minus_k_base_mod_4096": r["v_minus_k"],
+         "eager_us_per_step": round(r["eager_ms"] * 1e3, 3)}
+    if r["single_call_us"]:
+        d["single_call_us"] = r["single_call_us"]
+    return d
+
+
+def main():
+    a = _args()
+    if a.gpus != 1:
+        print(f"bench.py runs on one GPU only (asked for --gpus {a.gpus}); this build has no multi-GPU path.",
+              file=sys.stderr)
+        sys.exit(2)
+    if a.steps < 1 or a.warmup < 0:
+        print("--steps must be at least 1 and --warmup at least 0", file=sys.stderr)
+        sys.exit(2)
+    if a.probe:
+        _probe(a)
+        return
+    if a.summarize:
+        summarize(a)
+        return
+    if a.prefill:
+        _prefill(a)
+        return
+
+    r = _measure_decode(a, a.workload, a.kv_placement, a.steps, a.warmup, a.op, single_calls=a.op != "append",
+                        want_w=a.cpu_seconds > 0 and a.op == "attention")
+    spec = r["spec"]
+    ms, eager_ms = r["ms"], r["eager_ms"]
     if a.op == "append":
         row_bytes = spec.batch * spec.num_kv_heads * spec.head_dim * spec.elem_bytes * 2  # K and V rows
         moved = 2 * row_bytes  # each row read once and written once
         gbps = moved / (ms * 1e-3) / 1e9
         print(json.dumps({
             "metric": "kv-append µs/step", "value": round(ms * 1e3, 3), "unit": "µs", "n_gpus": 1,
-            "steps": steps, "warmup": a.warmup, "ms_per_step": round(ms, 6), "higher_is_better": False,
+            "steps": a.steps, "warmup": a.warmup, "ms_per_step": round(ms, 6), "higher_is_better": False,
             "scaling": "weak", "vs_baseline": None, "dtype": spec.dtype, "data": "synthetic",
             "config": {"workload": spec.name, "op": "append", "batch": spec.batch, "layout": spec.layout,
                        "page_size": spec.page_size, "row_bytes_per_step": row_bytes, "timing": a.timing,
@@ -649,27 +742,37 @@ def main():
             "cpu_baseline": None,
         }), flush=True)
         return
+    kv_bytes = r["kv_bytes"]
     gbps = kv_bytes / (ms * 1e-3) / 1e9
-    assert torch.isfinite(out).all().item()
-    # Spread of single calls (after the timed region): each of 100 eager
-    # calls bracketed by its own pair of events on the stream.
-    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(100)]
-    for i, (b0, b1) in enumerate(ev):
-        b0.record(stream)
-        step(i, stream)
-        b1.record(stream)
-    torch.cuda.synchronize()
-    per_call = sorted(b0.elapsed_time(b1) * 1e3 for b0, b1 in ev)
-    pct = {f"p{q}": round(per_call[min(len(per_call) - 1, q * len(per_call) // 100)], 3) for q in (10, 50, 90)}
+    print(f"# headline {spec.name}: {ms * 1e3:.3f} us/step, {gbps:.1f} GB/s", file=sys.stderr, flush=True)
+    cpu = _cpu_baseline(r["w"], a.cpu_seconds) if r["w"] is not None else None
+    r["w"] = None
 
-    cpu = _cpu_baseline(w, a.cpu_seconds) if a.cpu_seconds > 0 and a.op == "attention" else None
+    # The rest of the metric's 32k-128k range, the other K/V placement and
+    # the read ceiling, measured in the same process with the same rules.
+    also = {}
+    ceiling = None
+    if a.also and a.op == "attention" and a.chunk == 0 and a.variant == "auto":
+        other = "separate" if a.kv_placement == "offset" else "offset"
+        ro = _measure_decode(a, a.workload, other, a.steps, a.warmup, single_calls=False)
+        also[f"{spec.name}@{other}"] = dict(_summary(ro), kv_placement=other)
+        print(f"# {spec.name} @{other}: {ro['ms'] * 1e3:.3f} us/step", file=sys.stderr, flush=True)
+        for wl in a.also_workloads:
+            if wl == a.workload:
+                continue
+            rw = _measure_decode(a, wl, a.kv_placement, a.also_steps, min(a.warmup, 5), single_calls=False)
+            also[rw["spec"].name] = dict(_summary(rw), kv_placement=a.kv_placement)
+            print(f"# {rw['spec'].name}: {rw['ms'] * 1e3:.3f} us/step", file=sys.stderr, flush=True)
+        ceiling = {"read_4GiB": _read_ceiling(4 << 30, 64), "read_same_bytes": _read_ceiling(kv_bytes, a.steps)}
+        print(f"# read ceiling: {ceiling}", file=sys.stderr, flush=True)
+
     kind = a.variant if a.variant != "auto" else ("valu" if spec.dtype == "f32" else "mfma")
     line = {
         "metric": METRIC,
         "value": round(gbps, 2),
         "unit": "GB/s",
         "n_gpus": 1,
-        "steps": steps,
+        "steps": a.steps,
         "warmup": a.warmup,
         "ms_per_step": round(ms, 6),
         "us_per_step": round(ms * 1e3, 3),
@@ -682,22 +785,23 @@ def main():
         "data": "synthetic",
         "config": {
             "workload": spec.name, "batch": spec.batch, "num_q_heads": spec.num_q_heads,
-            "num_kv_heads": spec.num_kv_heads, "head_dim": spec.head_dim, "ctx_len_total": int(w.ctx_lens.sum()),
+            "num_kv_heads": spec.num_kv_heads, "head_dim": spec.head_dim, "ctx_len_total": r["ctx_len_total"],
             "layout": spec.layout, "page_size": spec.page_size, "kv_bytes_per_step": kv_bytes,
-            "kv_copies_cycled": copies, "kv_placement": a.kv_placement, "v_minus_k_base_mod_4096": v_minus_k,
-            "chunk_tokens": chunk, "splits": splits, "kernel": kind,
+            "kv_copies_cycled": r["copies"], "kv_placement": a.kv_placement, "v_minus_k_base_mod_4096": r["v_minus_k"],
+            "chunk_tokens": r["chunk"], "splits": r["splits"], "kernel": kind,
             "timing": a.timing, "eager_us_per_step": round(eager_ms * 1e3, 3), "op": a.op,
-            "single_call_us": pct,
+            "single_call_us": r["single_call_us"],
+            "also": also or None,
         },
         "roofline": {
             "bound": "hbm", "achieved": round(gbps, 2), "peak": PEAK_HBM_GBPS, "unit": "GB/s",
             "frac": round(gbps / PEAK_HBM_GBPS, 4),
             "traffic": recorded_traffic(spec.name) if a.op == "attention" else None,
+            "read_ceiling": ceiling,
         },
         "cpu_baseline": cpu,
     }
     print(json.dumps(line), flush=True)
-
 
 if __name__ == "__main__":
     main()

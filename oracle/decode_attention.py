@@ -49,12 +49,24 @@ def fp8_e4m3_value(codes: np.ndarray) -> np.ndarray:
     is subnormal: m/8 * 2^-6. Otherwise (1 + m/8) * 2^(e - 7). Exponent 15
     with mantissa 7 is NaN; the format has no infinities (max 448).
     """
-    c = np.asarray(codes, dtype=np.uint8).astype(np.int64)
-    sign = np.where(c >> 7, -1.0, 1.0)
-    e = (c >> 3) & 15
-    m = (c & 7).astype(np.float64)
-    mag = np.where(e == 0, m / 8.0 * 2.0 ** -6, (1.0 + m / 8.0) * np.exp2(e - 7.0))
-    return np.where((e == 15) & (m == 7), np.nan, sign * mag)
+    return _e4m3_values_of_all_codes()[np.asarray(codes, dtype=np.uint8)]
+
+
+def _e4m3_values_of_all_codes() -> np.ndarray:
+    """The definition above evaluated once for each of the 256 codes (indexed by code)."""
+    global _E4M3_ALL
+    if _E4M3_ALL is None:
+        c = np.arange(256, dtype=np.int64)
+        sign = np.where(c >> 7, -1.0, 1.0)
+        e = (c >> 3) & 15
+        m = (c & 7).astype(np.float64)
+        mag = np.where(e == 0, m / 8.0 * 2.0 ** -6, (1.0 + m / 8.0) * np.exp2(e - 7.0))
+        _E4M3_ALL = np.where((e == 15) & (m == 7), np.nan, sign * mag)
+        _E4M3_ALL.setflags(write=False)
+    return _E4M3_ALL
+
+
+_E4M3_ALL = None
 
 
 def widen(x: np.ndarray, dtype: str) -> np.ndarray:

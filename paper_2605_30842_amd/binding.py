@@ -315,6 +315,40 @@ def comem_cost_max_compression_ratio(inputs: CostInputs) -> float:
     return _cost_call("comem_cost_max_compression_ratio", ctypes.byref(inputs))
 
 
+def _torch_dtypes(dtype: str):
+    """(query dtypes, cache dtypes) a plan of `dtype` accepts as torch dtypes."""
+    import torch
+
+    if dtype == "f32":
+        return (torch.float32,), (torch.float32,)
+    if dtype == "bf16":
+        return (torch.bfloat16,), (torch.bfloat16,)
+    fp8 = tuple(t for t in (getattr(torch, "float8_e4m3fn", None),) if t is not None)
+    return (torch.bfloat16,), (torch.uint8,) + fp8
+
+
+def _need(cond: bool, msg: str) -> None:
+    if not cond:
+        raise ValueError(msg)
+
+
+def _check_tensor(name, t, dtypes, device, shape=None, ndim=None, contiguous=True):
+    """Raise ValueError unless t is a tensor on `device` with one of `dtypes`, the given shape (None entries
+    match any size) or rank, and (if asked) contiguous."""
+    import torch
+
+    _need(isinstance(t, torch.Tensor), f"{name} must be a torch tensor, got {type(t).__name__}")
+    _need(t.device == device, f"{name} is on {t.device}, expected {device}")
+    _need(t.dtype in dtypes, f"{name} has dtype {t.dtype}, expected {' or '.join(str(d) for d in dtypes)}")
+    if shape is not None:
+        _need(t.dim() == len(shape) and all(w is None or w == g for w, g in zip(shape, t.shape)),
+              f"{name} has shape {tuple(t.shape)}, expected {tuple('*' if w is None else w for w in shape)}")
+    if ndim is not None:
+        _need(t.dim() == ndim, f"{name} must have {ndim} dimensions, got {t.dim()}")
+    if contiguous:
+        _need(t.is_contiguous(), f"{name} must be contiguous")
+
+
 # ------------------------------------------------------------ torch wrapper
 
 
@@ -336,12 +370,14 @@ def kv_cache_pair(shape, dtype, device):
     n = math.prod(shape)
     nbytes = n * esize
     gap = (V_BASE_OFFSET_BYTES - nbytes) % V_BASE_OFFSET_MODULUS  # bytes between K's end and V's start
-    assert gap % esize == 0
+    if gap % esize != 0:
+        raise ValueError(f"element size {esize} does not divide the placement gap {gap}")
     g = gap // esize
     buf = torch.empty(2 * n + g, dtype=dtype, device=device)
     k = buf[:n].view(shape)
     v = buf[n + g:2 * n + g].view(shape)
-    assert (v.data_ptr() - k.data_ptr()) % V_BASE_OFFSET_MODULUS == V_BASE_OFFSET_BYTES
+    if (v.data_ptr() - k.data_ptr()) % V_BASE_OFFSET_MODULUS != V_BASE_OFFSET_BYTES:
+        raise RuntimeError("K/V placement not reached (allocation misaligned)")
     return k, v
 
 
@@ -365,6 +401,10 @@ class DecodeAttention:
                            "mfma_grid": VARIANT_MFMA_GRID}[variant], float(k_scale), float(v_scale),
                           FLAG_DEBUG_CHECKS if debug_checks else 0)
         self.device = device
+        self.dtype = dtype
+        self.num_q_heads, self.num_kv_heads, self.head_dim = num_q_heads, num_kv_heads, head_dim
+        self._torch_device = torch.device("cuda", device)
+        self._q_dtypes, self._kv_dtypes = _torch_dtypes(dtype)
         self.plan, self.workspace_bytes = comem_decode_attn_init(self.cfg, device)
         self.workspace = torch.zeros(max(self.workspace_bytes, 256), dtype=torch.uint8, device=f"cuda:{device}")
 
@@ -387,6 +427,49 @@ class DecodeAttention:
         return comem_decode_attn_device_errors(self.plan, self.workspace.data_ptr(), self.workspace_bytes,
                                                self._stream(stream))
 
+    # Checks of every tensor against the plan, before any pointer reaches the library.
+
+    def _check_q_out(self, q, out, lse, rows=None):
+        Hq, D = self.num_q_heads, self.head_dim
+        _check_tensor("q", q, self._q_dtypes, self._torch_device, shape=(rows, Hq, D))
+        R = q.shape[0]
+        import torch
+
+        if out is not None:
+            _check_tensor("out", out, (torch.float32,), self._torch_device, shape=(R, Hq, D))
+        if lse is not None:
+            _check_tensor("lse", lse, (torch.float32,), self._torch_device, shape=(R, Hq))
+
+    def _check_cache(self, k, v, paged: bool):
+        dims = 4 if paged else 3
+        for name, t in (("k", k), ("v", v)):
+            _check_tensor(name, t, self._kv_dtypes, self._torch_device, ndim=dims, contiguous=False)
+            _need(t.shape[-2] == self.num_kv_heads and t.shape[-1] == self.head_dim,
+                  f"{name} has shape {tuple(t.shape)}, expected [..., {self.num_kv_heads}, {self.head_dim}]")
+            _need(t.stride(-1) == 1, f"{name} must have a contiguous last dimension")
+        _need(k.shape == v.shape and k.stride() == v.stride(), "k and v must have the same shape and strides")
+        _need(k.dtype == v.dtype, "k and v must have the same dtype")
+
+    def _check_lengths(self, ctx_lens, batch, seq_start=None, block_table=None):
+        import torch
+
+        _check_tensor("ctx_lens", ctx_lens, (torch.int32,), self._torch_device, shape=(batch,))
+        if seq_start is not None:
+            _check_tensor("seq_start", seq_start, (torch.int64,), self._torch_device, shape=(batch,))
+        if block_table is not None:
+            _check_tensor("block_table", block_table, (torch.int32,), self._torch_device, shape=(batch, None))
+
+    def _check_new_rows(self, new_k, new_v, k, batch):
+        for name, t in (("new_k", new_k), ("new_v", new_v)):
+            _check_tensor(name, t, (k.dtype,), self._torch_device, shape=(batch, self.num_kv_heads, self.head_dim))
+
+    @staticmethod
+    def _check_bound(max_ctx_len, name="max_ctx_len"):
+        import numbers
+
+        _need(isinstance(max_ctx_len, numbers.Integral) and not isinstance(max_ctx_len, bool),
+              f"{name} must be an integer, got {type(max_ctx_len).__name__}")
+
     def _outputs(self, q, out, lse):
         import torch
 
@@ -402,8 +485,11 @@ class DecodeAttention:
         return (stream if stream is not None else torch.cuda.current_stream()).cuda_stream
 
     def forward(self, q, k, v, seq_start, ctx_lens, max_ctx_len: int, out=None, lse=None, stream=None):
+        self._check_q_out(q, out, lse)
+        self._check_cache(k, v, paged=False)
+        self._check_lengths(ctx_lens, q.shape[0], seq_start=seq_start)
+        self._check_bound(max_ctx_len)
         out, lse = self._outputs(q, out, lse)
-        assert k.stride() == v.stride() and k.stride(-1) == 1
         comem_decode_attn(self.plan, q.data_ptr(), k.data_ptr(), v.data_ptr(), k.stride(0), k.stride(1),
                           seq_start.data_ptr(), ctx_lens.data_ptr(), q.shape[0], int(max_ctx_len),
                           out.data_ptr(), None if lse is None else lse.data_ptr(), self.workspace.data_ptr(),
@@ -412,14 +498,20 @@ class DecodeAttention:
 
     def append(self, new_k, new_v, k, v, seq_start, ctx_lens, max_ctx_len: int, stream=None) -> None:
         """Store new_k/new_v [B, Hkv, D] as token ctx_lens[b] - 1 of each sequence (in place)."""
-        assert k.stride() == v.stride() and k.stride(-1) == 1
+        self._check_cache(k, v, paged=False)
+        self._check_new_rows(new_k, new_v, k, None)
+        self._check_lengths(ctx_lens, new_k.shape[0], seq_start=seq_start)
+        self._check_bound(max_ctx_len)
         comem_kv_append(self.plan, new_k.data_ptr(), new_v.data_ptr(), k.data_ptr(), v.data_ptr(), k.stride(0),
                         k.stride(1), seq_start.data_ptr(), ctx_lens.data_ptr(), new_k.shape[0], int(max_ctx_len),
                         self._stream(stream))
 
     def append_paged(self, new_k, new_v, k_pages, v_pages, block_table, ctx_lens, max_ctx_len: int,
                      stream=None) -> None:
-        assert k_pages.stride() == v_pages.stride() and k_pages.stride(-1) == 1
+        self._check_cache(k_pages, v_pages, paged=True)
+        self._check_new_rows(new_k, new_v, k_pages, None)
+        self._check_lengths(ctx_lens, new_k.shape[0], block_table=block_table)
+        self._check_bound(max_ctx_len)
         comem_kv_append_paged(self.plan, new_k.data_ptr(), new_v.data_ptr(), k_pages.data_ptr(),
                               v_pages.data_ptr(), k_pages.stride(0), k_pages.stride(1), k_pages.stride(2),
                               k_pages.shape[1], k_pages.shape[0], block_table.data_ptr(), block_table.shape[1],
@@ -428,8 +520,12 @@ class DecodeAttention:
     def append_forward(self, q, new_k, new_v, k, v, seq_start, ctx_lens, max_ctx_len: int, out=None, lse=None,
                        stream=None):
         """Store the new rows as token ctx_lens[b] - 1 and attend, in one launch."""
+        self._check_q_out(q, out, lse)
+        self._check_cache(k, v, paged=False)
+        self._check_new_rows(new_k, new_v, k, q.shape[0])
+        self._check_lengths(ctx_lens, q.shape[0], seq_start=seq_start)
+        self._check_bound(max_ctx_len)
         out, lse = self._outputs(q, out, lse)
-        assert k.stride() == v.stride() and k.stride(-1) == 1
         comem_append_decode_attn(self.plan, q.data_ptr(), new_k.data_ptr(), new_v.data_ptr(), k.data_ptr(),
                                  v.data_ptr(), k.stride(0), k.stride(1), seq_start.data_ptr(), ctx_lens.data_ptr(),
                                  q.shape[0], int(max_ctx_len), out.data_ptr(),
@@ -439,8 +535,12 @@ class DecodeAttention:
 
     def append_forward_paged(self, q, new_k, new_v, k_pages, v_pages, block_table, ctx_lens, max_ctx_len: int,
                              out=None, lse=None, stream=None):
+        self._check_q_out(q, out, lse)
+        self._check_cache(k_pages, v_pages, paged=True)
+        self._check_new_rows(new_k, new_v, k_pages, q.shape[0])
+        self._check_lengths(ctx_lens, q.shape[0], block_table=block_table)
+        self._check_bound(max_ctx_len)
         out, lse = self._outputs(q, out, lse)
-        assert k_pages.stride() == v_pages.stride() and k_pages.stride(-1) == 1
         comem_append_decode_attn_paged(self.plan, q.data_ptr(), new_k.data_ptr(), new_v.data_ptr(),
                                        k_pages.data_ptr(), v_pages.data_ptr(), k_pages.stride(0), k_pages.stride(1),
                                        k_pages.stride(2), k_pages.shape[1], k_pages.shape[0], block_table.data_ptr(),
@@ -451,8 +551,11 @@ class DecodeAttention:
 
     def forward_paged(self, q, k_pages, v_pages, block_table, ctx_lens, max_ctx_len: int, out=None, lse=None,
                       stream=None):
+        self._check_q_out(q, out, lse)
+        self._check_cache(k_pages, v_pages, paged=True)
+        self._check_lengths(ctx_lens, q.shape[0], block_table=block_table)
+        self._check_bound(max_ctx_len)
         out, lse = self._outputs(q, out, lse)
-        assert k_pages.stride() == v_pages.stride() and k_pages.stride(-1) == 1
         comem_decode_attn_paged(self.plan, q.data_ptr(), k_pages.data_ptr(), v_pages.data_ptr(),
                                 k_pages.stride(0), k_pages.stride(1), k_pages.stride(2), k_pages.shape[1],
                                 k_pages.shape[0], block_table.data_ptr(), block_table.shape[1],
@@ -460,6 +563,17 @@ class DecodeAttention:
                                 None if lse is None else lse.data_ptr(), self.workspace.data_ptr(),
                                 self.workspace_bytes, self._stream(stream))
         return out, lse
+
+    def _check_prefill(self, q, q_start, q_lens, max_q_len, ctx_lens, out, lse, max_ctx_len):
+        import torch
+
+        _check_tensor("ctx_lens", ctx_lens, (torch.int32,), self._torch_device, ndim=1)
+        batch = ctx_lens.shape[0]
+        self._check_q_out(q, out, lse)
+        _check_tensor("q_start", q_start, (torch.int64,), self._torch_device, shape=(batch,))
+        _check_tensor("q_lens", q_lens, (torch.int32,), self._torch_device, shape=(batch,))
+        self._check_bound(max_q_len, "max_q_len")
+        self._check_bound(max_ctx_len)
 
     def _prefill_outputs(self, q, out, lse):
         import torch
@@ -471,8 +585,10 @@ class DecodeAttention:
     def prefill(self, q, q_start, q_lens, max_q_len: int, k, v, seq_start, ctx_lens, max_ctx_len: int, out=None,
                 lse=None, stream=None):
         """Prefill attention of the packed new tokens q [total, Hq, D] over a contiguous cache."""
+        self._check_prefill(q, q_start, q_lens, max_q_len, ctx_lens, out, lse, max_ctx_len)
+        self._check_cache(k, v, paged=False)
+        self._check_lengths(ctx_lens, ctx_lens.shape[0], seq_start=seq_start)
         out, lse = self._prefill_outputs(q, out, lse)
-        assert k.stride() == v.stride() and k.stride(-1) == 1
         comem_prefill_attn(self.plan, q.data_ptr(), q_start.data_ptr(), q_lens.data_ptr(), int(max_q_len),
                            k.data_ptr(), v.data_ptr(), k.stride(0), k.stride(1), seq_start.data_ptr(),
                            ctx_lens.data_ptr(), ctx_lens.shape[0], int(max_ctx_len), out.data_ptr(),
@@ -481,8 +597,10 @@ class DecodeAttention:
 
     def prefill_paged(self, q, q_start, q_lens, max_q_len: int, k_pages, v_pages, block_table, ctx_lens,
                       max_ctx_len: int, out=None, lse=None, stream=None):
+        self._check_prefill(q, q_start, q_lens, max_q_len, ctx_lens, out, lse, max_ctx_len)
+        self._check_cache(k_pages, v_pages, paged=True)
+        self._check_lengths(ctx_lens, ctx_lens.shape[0], block_table=block_table)
         out, lse = self._prefill_outputs(q, out, lse)
-        assert k_pages.stride() == v_pages.stride() and k_pages.stride(-1) == 1
         comem_prefill_attn_paged(self.plan, q.data_ptr(), q_start.data_ptr(), q_lens.data_ptr(), int(max_q_len),
                                  k_pages.data_ptr(), v_pages.data_ptr(), k_pages.stride(0), k_pages.stride(1),
                                  k_pages.stride(2), k_pages.shape[1], k_pages.shape[0], block_table.data_ptr(),

@@ -1,10 +1,9 @@
 """The five named workloads at full size, in the launch configuration the bench
 times (automatic split plan, matrix-core kernel for bf16).
 
-The 2048-token fp32 and 32768-token bf16 workloads are checked on every
-output; the three multi-GB workloads on a sample of (sequence, query head)
-rows that the oracle computes one by one, always including the longest and
-shortest sequence and the first and last head of a GQA group.
+Every output and every lse of each workload is compared with the oracle's
+whole-batch result (the multi-GB workloads included: the oracle streams one
+(sequence, KV head) slice at a time and finishes them in seconds).
 """
 
 import numpy as np
@@ -17,22 +16,16 @@ from workloads.synth import WORKLOADS, generate
 pytestmark = pytest.mark.gpu
 
 
-def _rows(w, n, seed):
-    s = w.spec
-    r = np.random.default_rng(seed)
-    lens = w.ctx_lens
-    picks = {(int(np.argmax(lens)), 0), (int(np.argmax(lens)), s.num_q_heads - 1),
-             (int(np.argmin(lens)), s.group - 1), (int(np.argmin(lens)), s.group)}
-    while len(picks) < n:
-        picks.add((int(r.integers(s.batch)), int(r.integers(s.num_q_heads))))
-    return sorted(picks)
-
-
-@pytest.mark.parametrize("i", [1, 2])
+@pytest.mark.parametrize("i", [1, 2, 3, 4, 5])
 def test_full_workload_every_output(i):
+    import torch
+
     w = generate(WORKLOADS[i])
-    say(f"case full workload {i} {w.spec.name}")
-    out, lse = run(DeviceWorkload(w), make_op(w.spec))
+    say(f"case full workload {i} {w.spec.name} kv_bytes={w.kv_bytes}")
+    dw = DeviceWorkload(w)
+    out, lse = run(dw, make_op(w.spec))
+    del dw
+    torch.cuda.empty_cache()
     ro, rl = da.reference(w)
     err = check(out, lse, ro, rl, w.spec.dtype, w.spec.name)
     say(f"  max |err| {err:.3e}")
@@ -53,23 +46,3 @@ def test_headline_workload_repeated_calls_bitwise():
     for k in range(24):
         again = run(dw, op)
         assert np.array_equal(first[0], again[0]) and np.array_equal(first[1], again[1]), f"call {k + 1}"
-
-
-@pytest.mark.parametrize("i", [3, 4, 5])
-def test_full_workload_sampled_rows(i):
-    import torch
-
-    w = generate(WORKLOADS[i])
-    say(f"case full workload {i} {w.spec.name} kv_bytes={w.kv_bytes}")
-    dw = DeviceWorkload(w)
-    out, lse = run(dw, make_op(w.spec))
-    del dw
-    torch.cuda.empty_cache()
-    rows = _rows(w, 24, seed=i)
-    ref = da.decode_attention_rows(w, rows)
-    got_o = np.stack([out[b, h] for b, h in rows])
-    got_l = np.array([lse[b, h] for b, h in rows])
-    err = check(got_o, got_l, np.stack([o for o, _ in ref]), np.array([l for _, l in ref]), "bf16",
-                w.spec.name)
-    assert np.all(np.isfinite(out)) and np.all(np.isfinite(lse))
-    say(f"  max |err| over {len(rows)} rows {err:.3e}")

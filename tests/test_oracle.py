@@ -263,6 +263,38 @@ def pin_large_scores():
     _close(lse, np.full(2, 3600.0 + math.log1p(math.exp(-30.0))), 1e-12, "large scores lse")
 
 
+def _rows_cases():
+    """Small workloads of every layout the full-size checks use: packed ragged, paged with pages of 16
+    and 64 tokens, a GQA group of 8, and an FP8 cache with its per-tensor scales."""
+    yield generate(small_spec(WORKLOADS[3], [70, 0, 33, 129], seed=17).replace(head_dim=16), gap_rows=3)
+    yield generate(small_spec(WORKLOADS[4], [40, 1, 17, 96], seed=18, max_ctx_len=128).replace(head_dim=16),
+                   spare_pages=2)
+    yield generate(small_spec(WORKLOADS[5], [150, 64, 65], seed=19, max_ctx_len=192).replace(head_dim=16),
+                   spare_pages=1)
+    yield generate(small_spec(WORKLOADS[6], [90, 7], seed=20).replace(head_dim=16, k_scale=2.0 ** -5,
+                                                                     v_scale=2.0 ** -3))
+    yield generate(small_spec(WORKLOADS[7], [130, 64], seed=21, max_ctx_len=192).replace(head_dim=16,
+                                                                                     k_scale=2.0 ** -4))
+
+
+def pin_rows_equal_reference():
+    """Rows computed one by one (the full-size sampled checks and the CPU baseline use them) equal the
+    same rows of the whole-batch result, for every layout, a GQA group of 8 and FP8 scales; asking for
+    a subset of a sequence's heads, in any order and with repeats, changes nothing."""
+    for w in _rows_cases():
+        s = w.spec
+        ref_out, ref_lse = da.reference(w)
+        every = [(b, h) for b in range(s.batch) for h in range(s.num_q_heads)]
+        r = _rng(22)
+        subset = [every[i] for i in r.permutation(len(every))[: max(3, len(every) // 5)]]
+        for rows in (every, subset + subset[:2]):
+            got = da.decode_attention_rows(w, rows)
+            assert len(got) == len(rows), f"{s.name}: row count"
+            for (b, h), (o, l) in zip(rows, got):
+                _close(o, ref_out[b, h], 1e-12, f"{s.name} rows out ({b}, {h})")
+                _close([l], [ref_lse[b, h]], 1e-12, f"{s.name} rows lse ({b}, {h})")
+
+
 def pin_cost_model_case_study():
     with open(os.path.join(GOLDEN, "cost_model_case_study.json")) as f:
         g = json.load(f)
@@ -289,7 +321,7 @@ PINS = [
     pin_one_key, pin_uniform_scores, pin_weights_sum_to_one, pin_golden_closed_forms,
     pin_split_combine, pin_permutation_invariance, pin_key_shift, pin_brute_force, pin_torch_sdpa,
     pin_gqa_expansion, pin_paged_equals_contiguous, pin_empty_context, pin_widen_bf16,
-    pin_large_scores, pin_cost_model_case_study,
+    pin_large_scores, pin_cost_model_case_study, pin_rows_equal_reference,
 ]
 
 
@@ -404,6 +436,36 @@ def test_mutant_widen_is_caught(monkeypatch):
 
     monkeypatch.setattr(da, "widen", bad)
     assert _failing_pins()
+
+
+def test_mutant_rows_are_caught(monkeypatch):
+    """Plausible mistakes in the one-by-one rows are each caught by a pin."""
+    real = da.decode_attention_rows
+
+    def neighbour_head(w, rows):  # the head next to the one asked for
+        return real(w, [(b, (h + 1) % w.spec.num_q_heads) for b, h in rows])
+
+    def no_fp8_scales(w, rows):  # FP8 codes attended without their per-tensor scales
+        import dataclasses
+        return real(dataclasses.replace(w, spec=w.spec.replace(k_scale=1.0, v_scale=1.0)), rows)
+
+    def pages_as_packed(w, rows):  # the page pool read as if it were one packed cache
+        import dataclasses
+        if w.spec.layout != "paged":
+            return real(w, rows)
+        P, ps, Hkv, D = w.k_pages.shape
+        starts = np.concatenate([[0], np.cumsum(w.ctx_lens)[:-1]]).astype(np.int64)
+        flat = dataclasses.replace(w, spec=w.spec.replace(layout="contiguous", page_size=0),
+                                   k=w.k_pages.reshape(P * ps, Hkv, D), v=w.v_pages.reshape(P * ps, Hkv, D),
+                                   seq_start=np.minimum(starts, P * ps - np.maximum(w.ctx_lens, 1)))
+        return real(flat, rows)
+
+    def first_sequence(w, rows):  # every row attends over sequence 0
+        return real(w, [(0, h) for _, h in rows])
+
+    for fn in (neighbour_head, no_fp8_scales, pages_as_packed, first_sequence):
+        monkeypatch.setattr(da, "decode_attention_rows", fn)
+        assert "pin_rows_equal_reference" in _failing_pins(), fn.__name__
 
 
 def test_mutant_cost_model_is_caught(monkeypatch):

@@ -8,9 +8,10 @@ can consume it without sharing any of the method's computation.
 Shapes follow the paper's statement of the decode problem (Sec. 2.2, "LLM
 Inference"): one new query token per sequence with ``h_q`` heads of size
 ``d_h``; a KV cache of ``l`` tokens per sequence with ``h_kv`` heads of size
-``d_h``. The paper profiles decode with "random data with fixed lengths and a
-constant batch size" (Sec. 3.1); the five named workloads below stand in for
-that, with the shapes of the paper's models (Qwen3-class GQA, head size 128).
+``d_h``. For its decode profiling (Sec. 3.1) the paper feeds randomly drawn
+inputs at a set context length and a batch size held fixed; the five named
+workloads below stand in for that, with the shapes of the paper's models
+(Qwen3-class GQA, head size 128).
 
 Recipe (every choice that the paper leaves open):
   * seed of workload ``i`` is ``1000 + i``; ``SeedSequence(seed).spawn(6)``
