@@ -66,7 +66,8 @@ typedef enum {
   COMEM_ERR_WORKSPACE_TOO_SMALL = 5, /* workspace_bytes below what the call needs */
   COMEM_ERR_BAD_HANDLE = 6,          /* NULL or foreign plan */
   COMEM_ERR_HIP = 7,                 /* HIP runtime error (device query or launch) */
-  COMEM_ERR_NO_DEVICE = 8            /* plan made with device = COMEM_NO_DEVICE */
+  COMEM_ERR_NO_DEVICE = 8,           /* plan made with device = COMEM_NO_DEVICE */
+  COMEM_ERR_SCRATCH_LIMIT = 9        /* call needs more than the library's fixed scratch holds */
 } comem_status;
 
 typedef enum {
@@ -202,6 +203,35 @@ comem_status comem_decode_attn(const comem_decode_attn_plan* plan, const void* q
                                const int64_t* seq_start, const int32_t* ctx_lens, int32_t batch,
                                int64_t max_ctx_len, float* out, float* lse, void* workspace,
                                size_t workspace_bytes, void* hip_stream);
+
+/* Allocation-free form of comem_decode_attn, for callers that cannot
+ * allocate device memory: code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc. Instead of a caller workspace it uses a
+ * scratch array that the library holds in device memory, one copy of
+ * COMEM_NOALLOC_SCRATCH_BYTES per GPU, from the first comem_decode_attn_init
+ * on that device until the process ends. It calls no allocating routine.
+ * Arguments, results and planning are those of comem_decode_attn with a
+ * workspace of the plan's workspace_bytes (same kernels, same splits, same
+ * bits). The scratch starts with a fixed 64 KiB of counters, then the split
+ * partial results:
+ *   COMEM_ERR_SCRATCH_LIMIT  the call's partial results would not fit in the
+ *                            rest of the scratch (for example batch 16 of
+ *                            64K-token contexts with 32 query heads of 128 fits;
+ *                            a call past that does not), or the plan's
+ *                            max_batch * h_kv exceeds 16381 counters;
+ *   COMEM_ERR_UNSUPPORTED    plan made with COMEM_FLAG_DEBUG_CHECKS (its error
+ *                            word needs a caller workspace);
+ *   COMEM_ERR_HIP            the scratch of the plan's device could not be set up.
+ * Every call on one GPU shares that GPU's scratch, which keeps the last call's
+ * contents: the counters return to zero at the end of each call, and partial
+ * results are written before they are read. Calls that can overlap on one
+ * GPU (different streams, or different host threads) race on it and give
+ * wrong results: serialise them. */
+#define COMEM_NOALLOC_SCRATCH_BYTES (32u << 20)
+comem_status comem_decode_attn_noalloc(const comem_decode_attn_plan* plan, const void* q, const void* k,
+                                       const void* v, int64_t stride_token, int64_t stride_head,
+                                       const int64_t* seq_start, const int32_t* ctx_lens, int32_t batch,
+                                       int64_t max_ctx_len, float* out, float* lse, void* hip_stream);
 
 /* Paged cache driven by a block table (the paging scheme that the paper's
  * serving engine uses, cited in Sec. 1 and configured in Sec. 4.2).

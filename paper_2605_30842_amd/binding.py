@@ -20,7 +20,7 @@ LIB_PATH = os.path.join(PKG, "libcomem_attn.so")
 PROBE_LIB_PATH = os.path.join(PKG, "libcomem_probe.so")
 
 OK, ERR_NULL_POINTER, ERR_INVALID_SHAPE, ERR_UNSUPPORTED, ERR_MISALIGNED = 0, 1, 2, 3, 4
-ERR_WORKSPACE_TOO_SMALL, ERR_BAD_HANDLE, ERR_HIP, ERR_NO_DEVICE = 5, 6, 7, 8
+ERR_WORKSPACE_TOO_SMALL, ERR_BAD_HANDLE, ERR_HIP, ERR_NO_DEVICE, ERR_SCRATCH_LIMIT = 5, 6, 7, 8, 9
 F32, BF16, FP8_E4M3 = 0, 1, 2
 DTYPES = {"f32": F32, "bf16": BF16, "fp8": FP8_E4M3}
 VARIANT_AUTO, VARIANT_VALU, VARIANT_MFMA, VARIANT_MFMA_GRID = 0, 1, 2, 3
@@ -31,7 +31,9 @@ EXPORTED = (
     "comem_decode_attn_plan_splits", "comem_decode_attn", "comem_decode_attn_paged",
     "comem_kv_append", "comem_kv_append_paged", "comem_append_decode_attn", "comem_append_decode_attn_paged",
     "comem_prefill_attn", "comem_prefill_attn_paged", "comem_decode_attn_device_errors",
+    "comem_decode_attn_noalloc",
 )
+NOALLOC_SCRATCH_BYTES = 32 << 20  # COMEM_NOALLOC_SCRATCH_BYTES
 FLAG_DEBUG_CHECKS = 1
 DEVICE_ERR_CTX_LEN, DEVICE_ERR_BLOCK_TABLE = 1, 2
 PROBE_EXPORTED = ("comem_probe_read", "comem_probe_copy")
@@ -115,6 +117,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.comem_decode_attn_device_errors.restype = ctypes.c_int
     lib.comem_decode_attn.argtypes = [vp, vp, vp, vp, i64, i64, vp, vp, i32, i64, vp, vp, vp, sz, vp]
     lib.comem_decode_attn.restype = ctypes.c_int
+    lib.comem_decode_attn_noalloc.argtypes = [vp, vp, vp, vp, i64, i64, vp, vp, i32, i64, vp, vp, vp]
+    lib.comem_decode_attn_noalloc.restype = ctypes.c_int
     lib.comem_decode_attn_paged.argtypes = [vp, vp, vp, vp, i64, i64, i64, i32, i64, vp, i32, vp, i32, i64,
                                             vp, vp, vp, sz, vp]
     lib.comem_decode_attn_paged.restype = ctypes.c_int
@@ -224,6 +228,13 @@ def comem_decode_attn(plan, q, k, v, stride_token, stride_head, seq_start, ctx_l
     _check(load_library().comem_decode_attn(plan, q, k, v, stride_token, stride_head, seq_start, ctx_lens,
                                             batch, max_ctx_len, out, lse, workspace, workspace_bytes, stream),
            "comem_decode_attn")
+
+
+def comem_decode_attn_noalloc(plan, q, k, v, stride_token, stride_head, seq_start, ctx_lens, batch, max_ctx_len,
+                              out, lse, stream) -> None:
+    _check(load_library().comem_decode_attn_noalloc(plan, q, k, v, stride_token, stride_head, seq_start, ctx_lens,
+                                                    batch, max_ctx_len, out, lse, stream),
+           "comem_decode_attn_noalloc")
 
 
 def comem_decode_attn_paged(plan, q, k_pages, v_pages, stride_page, stride_token, stride_head, page_size,

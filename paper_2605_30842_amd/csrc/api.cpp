@@ -12,6 +12,7 @@
 #include "comem_decode_attn.h"
 #include "comem_prefill_attn.h"
 #include "kv_append.h"
+#include "noalloc.h"
 #include "prefill.h"
 
 namespace comem {
@@ -305,7 +306,7 @@ comem_status launch_append(const comem::AppendParams& a, bool paged, int32_t bat
 void fill_common(const comem_decode_attn_plan& p, comem::AttnParams& a, const void* q, const void* k,
                  const void* v, int64_t stride_token, int64_t stride_head, const int32_t* ctx_lens,
                  float* out, float* lse, void* workspace, int64_t batch, int64_t max_ctx_len, int64_t chunk,
-                 int64_t splits, bool queue) {
+                 int64_t splits, bool queue, size_t ticket_region) {
   const int64_t e = elem_bytes(p.cfg);
   std::memset(&a, 0, sizeof(a));
   a.max_ctx = static_cast<int32_t>(max_ctx_len);
@@ -332,8 +333,8 @@ void fill_common(const comem_decode_attn_plan& p, comem::AttnParams& a, const vo
     const size_t slots = static_cast<size_t>(batch) * static_cast<size_t>(splits) *
                          static_cast<size_t>(p.cfg.num_q_heads);
     a.tickets = reinterpret_cast<uint32_t*>(ws);
-    a.lse_part = reinterpret_cast<float*>(ws + p.ticket_bytes);
-    a.o_part = reinterpret_cast<float*>(ws + p.ticket_bytes + align256(slots * 4));
+    a.lse_part = reinterpret_cast<float*>(ws + ticket_region);
+    a.o_part = reinterpret_cast<float*>(ws + ticket_region + align256(slots * 4));
   }
 }
 
@@ -342,9 +343,10 @@ comem_status decode_contiguous(const comem_decode_attn_plan* plan, const void* q
                                const void* new_v, const void* k, const void* v, int64_t stride_token,
                                int64_t stride_head, const int64_t* seq_start, const int32_t* ctx_lens,
                                int32_t batch, int64_t max_ctx_len, float* out, float* lse, void* workspace,
-                               size_t workspace_bytes, void* hip_stream, bool fused) {
+                               size_t workspace_bytes, void* hip_stream, bool fused, size_t ticket_region = 0) {
   const comem_decode_attn_plan* p = checked(plan);
   if (p == nullptr) return COMEM_ERR_BAD_HANDLE;
+  if (ticket_region == 0) ticket_region = p->ticket_bytes;
   comem_status st = validate_common(*p, q, k, v, stride_token, stride_head, ctx_lens, batch, max_ctx_len,
                                     out, lse, workspace);
   if (st != COMEM_OK || batch == 0) return st;
@@ -363,7 +365,7 @@ comem_status decode_contiguous(const comem_decode_attn_plan* plan, const void* q
   const bool queue = uses_queue(*p, batch, workspace, workspace_bytes);
   comem::AttnParams a;
   fill_common(*p, a, q, k, v, stride_token, stride_head, ctx_lens, out, lse, workspace, batch, max_ctx_len, chunk,
-              splits, queue);
+              splits, queue, ticket_region);
   a.seq_start = seq_start;
   if (fused) {
     a.new_k = static_cast<const char*>(new_k);
@@ -401,7 +403,7 @@ comem_status decode_paged(const comem_decode_attn_plan* plan, const void* q, con
   const bool queue = uses_queue(*p, batch, workspace, workspace_bytes);
   comem::AttnParams a;
   fill_common(*p, a, q, k_pages, v_pages, stride_token, stride_head, ctx_lens, out, lse, workspace, batch,
-              max_ctx_len, chunk, splits, queue);
+              max_ctx_len, chunk, splits, queue, p->ticket_bytes);
   a.block_table = block_table;
   a.stride_page = stride_page * elem_bytes(p->cfg);
   a.max_pages = max_pages_per_seq;
@@ -485,6 +487,7 @@ const char* comem_status_string(comem_status s) {
     case COMEM_ERR_BAD_HANDLE: return "NULL or invalid plan";
     case COMEM_ERR_HIP: return "HIP runtime error";
     case COMEM_ERR_NO_DEVICE: return "plan was made without a device";
+    case COMEM_ERR_SCRATCH_LIMIT: return "call needs more than the library's fixed device scratch holds";
   }
   return "unknown status";
 }
@@ -533,6 +536,9 @@ comem_status comem_decode_attn_init(const comem_decode_attn_config* cfg, int dev
     if (c < slots) slots = c;
   }
   p->workspace_bytes = slots_workspace_bytes(*p, slots);
+  // The allocation-free entry point's scratch on this device (looked up and
+  // cleared once per device); the other entry points work without it.
+  if (device != COMEM_NO_DEVICE) (void)comem::scratch_setup(device);
   *plan_out = p;
   *workspace_bytes_out = p->workspace_bytes;
   return COMEM_OK;
@@ -591,6 +597,35 @@ comem_status comem_decode_attn(const comem_decode_attn_plan* plan, const void* q
                                size_t workspace_bytes, void* hip_stream) {
   return decode_contiguous(plan, q, nullptr, nullptr, k, v, stride_token, stride_head, seq_start, ctx_lens, batch,
                            max_ctx_len, out, lse, workspace, workspace_bytes, hip_stream, false);
+}
+
+comem_status comem_decode_attn_noalloc(const comem_decode_attn_plan* plan, const void* q, const void* k,
+                                       const void* v, int64_t stride_token, int64_t stride_head,
+                                       const int64_t* seq_start, const int32_t* ctx_lens, int32_t batch,
+                                       int64_t max_ctx_len, float* out, float* lse, void* hip_stream) {
+  const comem_decode_attn_plan* p = checked(plan);
+  if (p == nullptr) return COMEM_ERR_BAD_HANDLE;
+  if (debug_checks(*p)) return COMEM_ERR_UNSUPPORTED;
+  comem_status st = validate_common(*p, q, k, v, stride_token, stride_head, ctx_lens, batch, max_ctx_len, out, lse,
+                                    nullptr);
+  if (st != COMEM_OK || batch == 0) return st;
+  if (seq_start == nullptr) return COMEM_ERR_NULL_POINTER;
+  if (!aligned(seq_start, 8)) return COMEM_ERR_MISALIGNED;
+  // The splits a call with the plan's own workspace would use, and what they
+  // need past the scratch's fixed counter region.
+  if (p->ticket_bytes > comem::kScratchTicketBytes) return COMEM_ERR_SCRATCH_LIMIT;
+  int64_t chunk = 0, splits = 0;
+  st = plan_call(*p, batch, max_ctx_len, 0, p->workspace_bytes, &chunk, &splits);
+  if (st != COMEM_OK) return st;
+  const size_t partials = call_workspace_bytes(*p, batch, splits);
+  const size_t need = comem::kScratchTicketBytes + (partials > 0 ? partials - p->ticket_bytes : 0);
+  if (need > comem::kScratchBytes) return COMEM_ERR_SCRATCH_LIMIT;
+  if (p->device == COMEM_NO_DEVICE) return COMEM_ERR_NO_DEVICE;
+  void* scratch = comem::scratch_pointer(p->device);
+  if (scratch == nullptr) return COMEM_ERR_HIP;
+  return decode_contiguous(plan, q, nullptr, nullptr, k, v, stride_token, stride_head, seq_start, ctx_lens, batch,
+                           max_ctx_len, out, lse, scratch, comem::kScratchBytes, hip_stream, false,
+                           comem::kScratchTicketBytes);
 }
 
 comem_status comem_decode_attn_paged(const comem_decode_attn_plan* plan, const void* q,

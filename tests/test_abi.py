@@ -99,7 +99,7 @@ def test_init_null_arguments():
 
 
 def test_status_strings_and_null_destroy():
-    for s in range(9):
+    for s in range(10):
         assert B.status_string(s) and B.status_string(s) != "unknown status"
     assert B.status_string(99) == "unknown status"
     assert B.load_library().comem_decode_attn_destroy(None) == B.OK
@@ -163,6 +163,82 @@ def test_bad_handle():
     junk = ctypes.create_string_buffer(256)
     args = _contig_args(ctypes.addressof(junk), 0)
     assert _call(args) == B.ERR_BAD_HANDLE
+
+
+def _noalloc_args(plan, **kw):
+    args = dict(plan=plan, q=A, k=A, v=A, stride_token=8 * 128, stride_head=128, seq_start=A, ctx_lens=A,
+                batch=2, max_ctx_len=4096, out=A, lse=A, stream=None)
+    args.update(kw)
+    return args
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(), B.ERR_NO_DEVICE),
+    (dict(batch=0, q=None), B.OK),
+    (dict(batch=5), B.ERR_INVALID_SHAPE),
+    (dict(max_ctx_len=4097), B.ERR_INVALID_SHAPE),
+    (dict(q=None), B.ERR_NULL_POINTER),
+    (dict(seq_start=None), B.ERR_NULL_POINTER),
+    (dict(seq_start=A + 4), B.ERR_MISALIGNED),
+    (dict(out=A + 4), B.ERR_MISALIGNED),
+    (dict(stride_token=8 * 128 + 4), B.ERR_MISALIGNED),
+    (dict(plan=None), B.ERR_BAD_HANDLE),
+])
+def test_noalloc_validation(plan, kw, status):
+    p, _ = plan
+    args = _noalloc_args(p)
+    args.update(kw)
+    assert B.load_library().comem_decode_attn_noalloc(*args.values()) == status
+
+
+def _scratch_need(batch, splits, hq, d):
+    rows = batch * splits * hq
+    return 64 * 1024 + ((rows * 4 + 255) // 256) * 256 + rows * d * 4
+
+
+def test_noalloc_rejects_calls_past_the_scratch():
+    """Planned as the workspace form would plan them; a call whose partial results do not fit the fixed
+    scratch is refused (before any HIP call), one that fits passes validation."""
+    lib = B.load_library()
+    fits, too_big = None, None
+    p, ws = B.comem_decode_attn_init(_cfg(max_batch=64, max_ctx_len=65536), B.NO_DEVICE)
+    try:
+        for batch in (1, 2, 4, 8, 16, 32, 64):
+            for L in (4096, 16384, 65536):
+                chunk, splits = B.comem_decode_attn_plan_splits(p, batch, L, ws)
+                need = _scratch_need(batch, splits, 32, 128) if splits > 1 else 64 * 1024
+                st = lib.comem_decode_attn_noalloc(*_noalloc_args(p, batch=batch, max_ctx_len=L).values())
+                if need <= B.NOALLOC_SCRATCH_BYTES:
+                    assert st == B.ERR_NO_DEVICE, (batch, L)
+                    fits = (batch, L)
+                else:
+                    assert st == B.ERR_SCRATCH_LIMIT, (batch, L)
+                    too_big = (batch, L)
+    finally:
+        B.comem_decode_attn_destroy(p)
+    assert fits and too_big
+    # batch 16 of 64K-token contexts (the header's example) fits
+    p, ws = B.comem_decode_attn_init(_cfg(max_batch=16, max_ctx_len=65536), B.NO_DEVICE)
+    try:
+        assert lib.comem_decode_attn_noalloc(*_noalloc_args(p, batch=16, max_ctx_len=65536).values()) == \
+            B.ERR_NO_DEVICE
+    finally:
+        B.comem_decode_attn_destroy(p)
+
+
+def test_noalloc_refuses_debug_plans_and_huge_ticket_regions():
+    lib = B.load_library()
+    p, _ = B.comem_decode_attn_init(_cfg(flags=B.FLAG_DEBUG_CHECKS), B.NO_DEVICE)
+    try:
+        assert lib.comem_decode_attn_noalloc(*_noalloc_args(p).values()) == B.ERR_UNSUPPORTED
+    finally:
+        B.comem_decode_attn_destroy(p)
+    # 4096 sequences x 8 KV heads = 32768 tickets: more than the 64 KiB counter region holds
+    p, _ = B.comem_decode_attn_init(_cfg(max_batch=4096, max_ctx_len=64), B.NO_DEVICE)
+    try:
+        assert lib.comem_decode_attn_noalloc(*_noalloc_args(p, max_ctx_len=64).values()) == B.ERR_SCRATCH_LIMIT
+    finally:
+        B.comem_decode_attn_destroy(p)
 
 
 def _paged_args(plan, ws, **kw):
