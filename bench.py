@@ -80,7 +80,7 @@ def _args():
                          "K/V caches, the other long-context workloads and the streaming-read ceiling)")
     ap.add_argument("--also-workloads", type=lambda s: [int(x) for x in s.split(",") if x], default=[3, 4, 5],
                     help="comma-separated workloads timed beside the headline (default 3,4,5)")
-    ap.add_argument("--also-steps", type=int, default=50, help="timed steps of each of those workloads")
+    ap.add_argument("--also-steps", type=int, default=200, help="timed steps of each of those workloads")
     ap.add_argument("--summarize", metavar="DIR", default=None,
                     help="write profiles/ summaries from rocprofv3 outputs under DIR (layout in summarize())")
     return ap.parse_args()
@@ -763,7 +763,7 @@ def main():
             rw = _measure_decode(a, wl, a.kv_placement, a.also_steps, min(a.warmup, 5), single_calls=False)
             also[rw["spec"].name] = dict(_summary(rw), kv_placement=a.kv_placement)
             print(f"# {rw['spec'].name}: {rw['ms'] * 1e3:.3f} us/step", file=sys.stderr, flush=True)
-        ceiling = {"read_4GiB": _read_ceiling(4 << 30, 64), "read_same_bytes": _read_ceiling(kv_bytes, a.steps)}
+        ceiling = {"read_4GiB": _read_ceiling(4 << 30, 160), "read_same_bytes": _read_ceiling(kv_bytes, a.steps)}
         print(f"# read ceiling: {ceiling}", file=sys.stderr, flush=True)
 
     kind = a.variant if a.variant != "auto" else ("valu" if spec.dtype == "f32" else "mfma")
