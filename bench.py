@@ -38,9 +38,10 @@ sys.path.insert(0, ROOT)
 PEAK_HBM_GBPS = 8000.0
 PEAK_BF16_TFLOPS = 2500.0  # MI355X dense bf16 matrix-core peak
 PROFILES = os.path.join(ROOT, "profiles")
-KERNEL_SOURCES = ["paper_2605_30842_amd/csrc/api.cpp", "paper_2605_30842_amd/csrc/attn_common.h",
+KERNEL_SOURCES = ["paper_2605_30842_amd/csrc/api.cpp", "paper_2605_30842_amd/csrc/plan.h",
+                  "paper_2605_30842_amd/csrc/attn_common.h",
                   "paper_2605_30842_amd/csrc/kernel_mfma.hip", "paper_2605_30842_amd/csrc/kernel_valu.hip"]
-PREFILL_SOURCES = ["paper_2605_30842_amd/csrc/api.cpp", "paper_2605_30842_amd/csrc/attn_common.h",
+PREFILL_SOURCES = ["paper_2605_30842_amd/csrc/api_prefill.cpp", "paper_2605_30842_amd/csrc/attn_common.h",
                    "paper_2605_30842_amd/csrc/prefill.h", "paper_2605_30842_amd/csrc/kernel_prefill.hip"]
 APPEND_SOURCES = ["paper_2605_30842_amd/csrc/api.cpp", "paper_2605_30842_amd/csrc/kv_append.h",
                   "paper_2605_30842_amd/csrc/kernel_append.hip"]

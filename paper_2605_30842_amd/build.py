@@ -17,7 +17,7 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB_NAME = "libcomem_attn.so"
-SOURCES = ["api.cpp", "kernel_mfma.hip", "kernel_valu.hip", "kernel_append.hip", "kernel_prefill.hip",
+SOURCES = ["api.cpp", "api_prefill.cpp", "kernel_mfma.hip", "kernel_valu.hip", "kernel_append.hip", "kernel_prefill.hip",
            "noalloc.hip", "cost_model.cpp"]
 PROBE_LIB_NAME = "libcomem_probe.so"
 PROBE_SOURCES = ["probe.hip"]

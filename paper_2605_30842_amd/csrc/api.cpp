@@ -10,10 +10,9 @@
 
 #include "attn_common.h"
 #include "comem_decode_attn.h"
-#include "comem_prefill_attn.h"
 #include "kv_append.h"
 #include "noalloc.h"
-#include "prefill.h"
+#include "plan.h"
 
 namespace comem {
 using KernelFn = void (*)(AttnParams);
@@ -25,43 +24,18 @@ int mfma_max_queue_batch();
 KernelFn select_valu_kernel(bool bf16, int head_dim, int group, bool paged);
 }  // namespace comem
 
+using namespace comem::host;
+
 namespace {
 
-constexpr uint64_t kPlanMagic = 0x434f4d454d444131ull;  // "COMEMDA1"
 constexpr int kAssumedCUs = 256;                        // gfx950 (MI355X) without a device query
 constexpr int64_t kTargetWgsPerCu = 2;                  // workgroups per compute unit for one full round
 constexpr int kQueueWgsPerCu = 2;                       // resident workgroups per compute unit (MFMA kernel)
 constexpr int64_t kTailRounds = 4;                      // items per resident workgroup that enable short last splits
 constexpr int64_t kMinChunk = 64;                       // tokens per split, lower bound
 constexpr int64_t kMaxChunk = 2048;                     // tokens per split, upper bound (auto plan)
-constexpr int64_t kMaxContext = int64_t{1} << 30;
-constexpr int kGridYZLimit = 65535;
-constexpr int64_t kMaxTokenStrideBytes = int64_t{1} << 26;  // lane offsets within a tile stay 32-bit
 
-size_t align256(size_t x) { return (x + 255) & ~size_t{255}; }
-int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
-bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) & (a - 1)) == 0; }
-
-}  // namespace
-
-struct comem_decode_attn_plan {
-  uint64_t magic;
-  comem_decode_attn_config cfg;
-  int device;
-  int num_cus;
-  size_t ticket_bytes;
-  size_t workspace_bytes;
-};
-
-namespace {
-
-int group_of(const comem_decode_attn_config& c) { return c.num_q_heads / c.num_kv_heads; }
 bool uses_mfma(const comem_decode_attn_plan& p);
-// Bytes of one K or V element (q is bf16 for FP8 caches).
-int elem_bytes(const comem_decode_attn_config& c) {
-  return c.dtype == COMEM_F32 ? 4 : (c.dtype == COMEM_FP8_E4M3 ? 1 : 2);
-}
-bool is_fp8(const comem_decode_attn_config& c) { return c.dtype == COMEM_FP8_E4M3; }
 
 // After the tickets [max_batch * Hkv]: the two work-queue counters and the
 // device error word.
@@ -167,50 +141,9 @@ comem_status validate_config(const comem_decode_attn_config& c) {
   return COMEM_OK;
 }
 
-const comem_decode_attn_plan* checked(const comem_decode_attn_plan* p) {
-  return (p != nullptr && p->magic == kPlanMagic) ? p : nullptr;
-}
 
-// Checks of the paged-layout arguments shared by attention and append.
-comem_status validate_paged(const comem_decode_attn_plan& p, int64_t stride_page, int32_t page_size,
-                            int64_t num_pages, const int32_t* block_table, int32_t max_pages_per_seq,
-                            int64_t max_ctx_len) {
-  if (block_table == nullptr) return COMEM_ERR_NULL_POINTER;
-  if (page_size <= 0 || page_size > 4096 || (page_size & (page_size - 1)) != 0) return COMEM_ERR_INVALID_SHAPE;
-  if (num_pages <= 0 || stride_page <= 0) return COMEM_ERR_INVALID_SHAPE;
-  if (max_pages_per_seq <= 0 || max_pages_per_seq < ceil_div(max_ctx_len, page_size))
-    return COMEM_ERR_INVALID_SHAPE;
-  if ((stride_page * elem_bytes(p.cfg)) % 16 != 0) return COMEM_ERR_MISALIGNED;
-  if (!aligned(block_table, 4)) return COMEM_ERR_MISALIGNED;
-  return COMEM_OK;
-}
 
-int log2_of(int32_t pow2) {
-  int shift = 0;
-  while ((1 << shift) < pow2) ++shift;
-  return shift;
-}
 
-// Checks shared by both compute calls.
-comem_status validate_common(const comem_decode_attn_plan& p, const void* q, const void* k, const void* v,
-                             int64_t stride_token, int64_t stride_head, const int32_t* ctx_lens,
-                             int32_t batch, int64_t max_ctx_len, const float* out, const float* lse,
-                             const void* workspace) {
-  if (batch < 0 || batch > p.cfg.max_batch) return COMEM_ERR_INVALID_SHAPE;
-  if (max_ctx_len < 0 || max_ctx_len > p.cfg.max_ctx_len) return COMEM_ERR_INVALID_SHAPE;
-  if (batch == 0) return COMEM_OK;
-  if (q == nullptr || k == nullptr || v == nullptr || ctx_lens == nullptr || out == nullptr)
-    return COMEM_ERR_NULL_POINTER;
-  if (stride_token <= 0 || stride_head < 0) return COMEM_ERR_INVALID_SHAPE;
-  if (p.cfg.num_kv_heads > 1 && stride_head == 0) return COMEM_ERR_INVALID_SHAPE;
-  const int64_t e = elem_bytes(p.cfg);
-  if ((stride_token * e) % 16 != 0 || (stride_head * e) % 16 != 0) return COMEM_ERR_MISALIGNED;
-  if (stride_token * e > kMaxTokenStrideBytes) return COMEM_ERR_INVALID_SHAPE;
-  if (!aligned(q, 16) || !aligned(k, 16) || !aligned(v, 16) || !aligned(out, 16)) return COMEM_ERR_MISALIGNED;
-  if (lse != nullptr && !aligned(lse, 4)) return COMEM_ERR_MISALIGNED;
-  if (workspace != nullptr && !aligned(workspace, 256)) return COMEM_ERR_MISALIGNED;
-  return COMEM_OK;
-}
 
 bool uses_mfma(const comem_decode_attn_plan& p) {
   return p.cfg.variant == COMEM_VARIANT_MFMA || p.cfg.variant == COMEM_VARIANT_MFMA_GRID ||
@@ -417,61 +350,6 @@ comem_status decode_paged(const comem_decode_attn_plan* plan, const void* q, con
   return launch(*p, true, a, batch, splits, queue, hip_stream);
 }
 
-// A prefill call with no sequence or no new token reads and writes nothing,
-// so, as for batch = 0 in the decode calls, it needs no buffers.
-bool prefill_is_empty(int32_t batch, int32_t max_q_len) { return batch == 0 || max_q_len == 0; }
-
-// Checks of a prefill call shared by both layouts; fills the kernel arguments.
-comem_status prepare_prefill(const comem_decode_attn_plan& p, const void* q, const int64_t* q_start,
-                             const int32_t* q_lens, int32_t max_q_len, const void* k, const void* v,
-                             int64_t stride_token, int64_t stride_head, const int32_t* ctx_lens, int32_t batch,
-                             int64_t max_ctx_len, float* out, float* lse, comem::PrefillParams& a) {
-  if (p.cfg.dtype != COMEM_BF16) return COMEM_ERR_UNSUPPORTED;
-  if (batch < 0 || batch > p.cfg.max_batch) return COMEM_ERR_INVALID_SHAPE;
-  if (max_ctx_len < 0 || max_ctx_len > p.cfg.max_ctx_len) return COMEM_ERR_INVALID_SHAPE;
-  if (max_q_len < 0 || max_q_len > max_ctx_len) return COMEM_ERR_INVALID_SHAPE;
-  if (prefill_is_empty(batch, max_q_len)) return COMEM_OK;
-  const comem_status st = validate_common(p, q, k, v, stride_token, stride_head, ctx_lens, batch, max_ctx_len, out,
-                                          lse, nullptr);
-  if (st != COMEM_OK) return st;
-  if (q_start == nullptr || q_lens == nullptr) return COMEM_ERR_NULL_POINTER;
-  if (!aligned(q_start, 8) || !aligned(q_lens, 4)) return COMEM_ERR_MISALIGNED;
-  const int64_t e = elem_bytes(p.cfg);
-  std::memset(&a, 0, sizeof(a));
-  a.q = static_cast<const char*>(q);
-  a.k = static_cast<const char*>(k);
-  a.v = static_cast<const char*>(v);
-  a.out = out;
-  a.lse = lse;
-  a.q_start = q_start;
-  a.q_lens = q_lens;
-  a.ctx_lens = ctx_lens;
-  a.stride_token = stride_token * e;
-  a.stride_head = stride_head * e;
-  a.num_q_heads = p.cfg.num_q_heads;
-  a.group = group_of(p.cfg);
-  a.tokens_per_block = comem::kPrefillRows / a.group;
-  a.scale_log2 = p.cfg.scale * 1.4426950408889634f;
-  a.max_ctx = static_cast<int32_t>(max_ctx_len);
-  a.max_q = max_q_len;
-  return COMEM_OK;
-}
-
-comem_status launch_prefill(const comem_decode_attn_plan& p, const comem::PrefillParams& a, bool paged,
-                            int32_t batch, int32_t max_q_len, void* stream) {
-  comem::PrefillKernelFn fn = comem::select_prefill_kernel(p.cfg.head_dim, paged ? a.page_mask + 1 : 0);
-  if (fn == nullptr) return COMEM_ERR_UNSUPPORTED;
-  const int64_t blocks = ceil_div(max_q_len, a.tokens_per_block);
-  comem::PrefillParams args = a;
-  void* argv[] = {&args};
-  const hipError_t err =
-      hipLaunchKernel(reinterpret_cast<const void*>(fn),
-                      dim3(static_cast<unsigned>(blocks), static_cast<unsigned>(p.cfg.num_kv_heads),
-                           static_cast<unsigned>(batch)),
-                      dim3(comem::kPrefillThreads), argv, 0, static_cast<hipStream_t>(stream));
-  return err == hipSuccess ? COMEM_OK : COMEM_ERR_HIP;
-}
-
 }  // namespace
 
 extern "C" {
@@ -660,49 +538,6 @@ comem_status comem_append_decode_attn_paged(const comem_decode_attn_plan* plan, 
   return decode_paged(plan, q, new_k, new_v, k_pages, v_pages, stride_page, stride_token, stride_head, page_size,
                       num_pages, block_table, max_pages_per_seq, ctx_lens, batch, max_ctx_len, out, lse, workspace,
                       workspace_bytes, hip_stream, true);
-}
-
-comem_status comem_prefill_attn(const comem_decode_attn_plan* plan, const void* q, const int64_t* q_start,
-                                const int32_t* q_lens, int32_t max_q_len, const void* k, const void* v,
-                                int64_t stride_token, int64_t stride_head, const int64_t* seq_start,
-                                const int32_t* ctx_lens, int32_t batch, int64_t max_ctx_len, float* out,
-                                float* lse, void* hip_stream) {
-  const comem_decode_attn_plan* p = checked(plan);
-  if (p == nullptr) return COMEM_ERR_BAD_HANDLE;
-  comem::PrefillParams a;
-  comem_status st = prepare_prefill(*p, q, q_start, q_lens, max_q_len, k, v, stride_token, stride_head, ctx_lens,
-                                    batch, max_ctx_len, out, lse, a);
-  if (st != COMEM_OK || prefill_is_empty(batch, max_q_len)) return st;
-  if (seq_start == nullptr) return COMEM_ERR_NULL_POINTER;
-  if (!aligned(seq_start, 8)) return COMEM_ERR_MISALIGNED;
-  if (p->device == COMEM_NO_DEVICE) return COMEM_ERR_NO_DEVICE;
-  a.seq_start = seq_start;
-  return launch_prefill(*p, a, false, batch, max_q_len, hip_stream);
-}
-
-comem_status comem_prefill_attn_paged(const comem_decode_attn_plan* plan, const void* q, const int64_t* q_start,
-                                      const int32_t* q_lens, int32_t max_q_len, const void* k_pages,
-                                      const void* v_pages, int64_t stride_page, int64_t stride_token,
-                                      int64_t stride_head, int32_t page_size, int64_t num_pages,
-                                      const int32_t* block_table, int32_t max_pages_per_seq,
-                                      const int32_t* ctx_lens, int32_t batch, int64_t max_ctx_len, float* out,
-                                      float* lse, void* hip_stream) {
-  const comem_decode_attn_plan* p = checked(plan);
-  if (p == nullptr) return COMEM_ERR_BAD_HANDLE;
-  comem::PrefillParams a;
-  comem_status st = prepare_prefill(*p, q, q_start, q_lens, max_q_len, k_pages, v_pages, stride_token, stride_head,
-                                    ctx_lens, batch, max_ctx_len, out, lse, a);
-  if (st != COMEM_OK || prefill_is_empty(batch, max_q_len)) return st;
-  st = validate_paged(*p, stride_page, page_size, num_pages, block_table, max_pages_per_seq, max_ctx_len);
-  if (st != COMEM_OK) return st;
-  if (p->device == COMEM_NO_DEVICE) return COMEM_ERR_NO_DEVICE;
-  a.block_table = block_table;
-  a.stride_page = stride_page * elem_bytes(p->cfg);
-  a.max_pages = max_pages_per_seq;
-  a.page_shift = log2_of(page_size);
-  a.page_mask = page_size - 1;
-  a.num_pages = num_pages;
-  return launch_prefill(*p, a, true, batch, max_q_len, hip_stream);
 }
 
 comem_status comem_kv_append(const comem_decode_attn_plan* plan, const void* new_k, const void* new_v,
