@@ -231,7 +231,7 @@ __device__ inline LaneOffsets<D> lane_offsets(int lane) {
 // One 64-key tile for the 32 rows of a wave. `limit` is the last key the
 // lane's row may see; MASKED is false when every key of the tile is visible
 // to every row of the workgroup.
-template <int D, bool MASKED>
+template <int D, bool MASKED, bool SAFE>
 __device__ inline void compute_tile(const TileBuf<D>& tb, int t0, int limit, int h, const LaneOffsets<D>& lo,
                                     const bf16x8 (&qop)[D / 16], float scale_log2, float& m_run, float& l_run,
                                     f32x16 (&acc)[D / 32]) {
@@ -272,15 +272,20 @@ __device__ inline void compute_tile(const TileBuf<D>& tb, int t0, int limit, int
   // Lazy maximum: move it only when some row would see a probability above
   // 2^kLazyMax. The first tile holds key 0, visible to every row, so the
   // maximum is finite from then on.
+  // With SAFE (the second half of a key-split workgroup, which starts in the
+  // middle of the keys) a row may have seen no key yet: its maximum is -inf,
+  // and its probabilities stay 0 until a visible key arrives.
   if (__builtin_amdgcn_ballot_w64((mt - m_run) * scale_log2 > kLazyMax) != 0) {
     const float m_new = fmaxf(m_run, mt);
-    const float alpha = fast_exp2((m_run - m_new) * scale_log2);
+    float alpha = fast_exp2((m_run - m_new) * scale_log2);
+    if constexpr (SAFE) alpha = m_new == -INFINITY ? 1.f : alpha;
 #pragma unroll
     for (int n = 0; n < NT; ++n) acc[n] *= alpha;
     l_run *= alpha;
     m_run = m_new;
   }
-  const float mb = m_run * scale_log2;
+  float mb = m_run * scale_log2;
+  if constexpr (SAFE) mb = m_run == -INFINITY ? 0.f : mb;
 
   float psum = 0.f;
 #pragma unroll
@@ -316,12 +321,16 @@ __device__ inline void compute_tile(const TileBuf<D>& tb, int t0, int limit, int
 // id to a work item itself (see the top of the kernel).
 constexpr int kXcds = 8;  // XCDs of the GPU; workgroups are dealt to them round robin
 
-template <int D, PLayout LAYOUT>
-__global__ __launch_bounds__(kPrefillThreads, 2) void prefill_mfma_kernel(const PrefillParams p) {
+// KH = 2 (a key-split workgroup, for grids of at most one workgroup per
+// compute unit): waves 4..7 take the same 128 rows as waves 0..3 over the
+// second half of the key tiles, with their own pair of LDS buffers, so each
+// SIMD holds two waves as it would with two workgroups per compute unit. The
+// halves merge their softmax states through LDS at the end.
+template <int D, PLayout LAYOUT, int KH>
+__global__ __launch_bounds__(kPrefillThreads * KH, KH == 1 ? 2 : 1) void prefill_mfma_kernel(const PrefillParams p) {
   constexpr int KS = D / 16;
   constexpr int NT = D / 32;
   constexpr bool PAGED = LAYOUT != PLayout::kContig;
-  __shared__ TileBuf<D> buf0, buf1;
   // Work item of the workgroup. Workgroups go to the XCDs in turn (linear
   // id modulo 8). When the (sequence, KV head) pairs divide evenly over the
   // XCDs, pair hb runs all its query blocks on XCD hb % 8, so the K/V tiles
@@ -337,9 +346,9 @@ __global__ __launch_bounds__(kPrefillThreads, 2) void prefill_mfma_kernel(const 
     const int x = lin % kXcds, k = lin / kXcds;
     const int r = k / gridDim.x;
     q = k - r * static_cast<int>(gridDim.x);
-    const int hb = x + kXcds * r;
-    b = hb / gridDim.y;
-    hk = hb - b * static_cast<int>(gridDim.y);
+    const int hbp = x + kXcds * r;
+    b = hbp / gridDim.y;
+    hk = hbp - b * static_cast<int>(gridDim.y);
   } else {
     b = blockIdx.z;
     hk = blockIdx.y;
@@ -364,7 +373,9 @@ __global__ __launch_bounds__(kPrefillThreads, 2) void prefill_mfma_kernel(const 
   const int nfree = (prefix + i0 + 1) / kPrefillTileKeys;  // tiles visible to every row
 
   const int lane = threadIdx.x & 63;
-  const int w = threadIdx.x >> 6;
+  const int wv = uniform_i32(threadIdx.x >> 6);
+  const int w = wv & 3;   // row group of the wave
+  const int kh = wv >> 2; // key half of the wave (0 unless KH = 2)
   const int j = lane & 31, h = lane >> 5;
   const int row = 32 * w + j;
   const int g = row / TB;
@@ -383,50 +394,125 @@ __global__ __launch_bounds__(kPrefillThreads, 2) void prefill_mfma_kernel(const 
   ld.page_shift = p.page_shift;
   ld.page_mask = p.page_mask;
   ld.kend = kend;
-  ld.init(uniform_i32(w), lane);
+  ld.init(w, lane);
 
-  ld.fetch_pages(0);
-  ld.load(buf0, 0);
-  if (ntiles > 1) ld.fetch_pages(kPrefillTileKeys);
-
-  // Q^T operand: row j, head_dim 16 ks + 8 h .. + 8.
+  // Q^T operand: row j, head_dim 16 ks + 8 h .. + 8 (requested after the first tile).
   bf16x8 qop[KS];
-  {
+  auto load_q = [&]() {
     const char* qrow = p.q + ((qs + ic) * p.num_q_heads + qh) * (D * 2);
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) qop[ks] = *reinterpret_cast<const bf16x8*>(qrow + 32 * ks + 16 * h);
-  }
+  };
   const LaneOffsets<D> lo = lane_offsets<D>(lane);
   f32x16 acc[NT];
 #pragma unroll
   for (int n = 0; n < NT; ++n) acc[n] = f32x16{};
   float m_run = -INFINITY, l_run = 0.f;
 
-  tile_loads_done();
-  __syncthreads();
-  // Tile t is in buffer t % 2 while tile t + 1 streams into the other one.
-  // Tiles before nfree are visible to every row whole; later ones take the
-  // causal mask. The loop handles two tiles per pass so that each half names
-  // its buffers statically.
-  auto step = [&](const TileBuf<D>& cur, TileBuf<D>& nxt, int t) {
-    if (t + 1 < ntiles) {
-      ld.load(nxt, kPrefillTileKeys * (t + 1));
-      if (t + 2 < ntiles) ld.fetch_pages(kPrefillTileKeys * (t + 2));
-    }
-    if (t < nfree) {
-      compute_tile<D, false>(cur, kPrefillTileKeys * t, limit, h, lo, qop, p.scale_log2, m_run, l_run, acc);
-    } else {
-      compute_tile<D, true>(cur, kPrefillTileKeys * t, limit, h, lo, qop, p.scale_log2, m_run, l_run, acc);
-    }
+  if constexpr (KH == 1) {
+    __shared__ TileBuf<D> buf0, buf1;
+    ld.fetch_pages(0);
+    ld.load(buf0, 0);
+    if (ntiles > 1) ld.fetch_pages(kPrefillTileKeys);
+    load_q();
     tile_loads_done();
     __syncthreads();
-  };
-  for (int t = 0; t < ntiles; t += 2) {
-    step(buf0, buf1, t);
-    if (t + 1 < ntiles) step(buf1, buf0, t + 1);
+    // Tile t is in buffer t % 2 while tile t + 1 streams into the other one.
+    // Tiles before nfree are visible to every row whole; later ones take the
+    // causal mask. The loop handles two tiles per pass so that each half
+    // names its buffers statically.
+    auto step = [&](const TileBuf<D>& cur, TileBuf<D>& nxt, int t) {
+      if (t + 1 < ntiles) {
+        ld.load(nxt, kPrefillTileKeys * (t + 1));
+        if (t + 2 < ntiles) ld.fetch_pages(kPrefillTileKeys * (t + 2));
+      }
+      if (t < nfree) {
+        compute_tile<D, false, false>(cur, kPrefillTileKeys * t, limit, h, lo, qop, p.scale_log2, m_run, l_run, acc);
+      } else {
+        compute_tile<D, true, false>(cur, kPrefillTileKeys * t, limit, h, lo, qop, p.scale_log2, m_run, l_run, acc);
+      }
+      tile_loads_done();
+      __syncthreads();
+    };
+    for (int t = 0; t < ntiles; t += 2) {
+      step(buf0, buf1, t);
+      if (t + 1 < ntiles) step(buf1, buf0, t + 1);
+    }
+    l_run += __shfl_xor(l_run, 32);
+  } else {
+    // Key half kh takes tiles [t_first, t_first + t_count) in `steps` steps
+    // (the same count in both halves, so that their barriers pair up), each
+    // half with its own pair of LDS buffers.
+    __shared__ TileBuf<D> bufs[2][2];
+    const int steps = (ntiles + 1) / 2;
+    const int t_first = kh * steps;
+    const int t_count = min(steps, ntiles - t_first);
+    TileBuf<D>& A = bufs[kh][0];
+    TileBuf<D>& B = bufs[kh][1];
+    if (t_count > 0) {
+      ld.fetch_pages(kPrefillTileKeys * t_first);
+      ld.load(A, kPrefillTileKeys * t_first);
+      if (t_count > 1) ld.fetch_pages(kPrefillTileKeys * (t_first + 1));
+    }
+    load_q();
+    tile_loads_done();
+    __syncthreads();
+    auto step = [&](const TileBuf<D>& cur, TileBuf<D>& nxt, int s) {
+      const int t = t_first + s;
+      if (s + 1 < t_count) {
+        ld.load(nxt, kPrefillTileKeys * (t + 1));
+        if (s + 2 < t_count) ld.fetch_pages(kPrefillTileKeys * (t + 2));
+      }
+      if (s < t_count) {
+        if (t < nfree) {
+          compute_tile<D, false, true>(cur, kPrefillTileKeys * t, limit, h, lo, qop, p.scale_log2, m_run, l_run, acc);
+        } else {
+          compute_tile<D, true, true>(cur, kPrefillTileKeys * t, limit, h, lo, qop, p.scale_log2, m_run, l_run, acc);
+        }
+      }
+      tile_loads_done();
+      __syncthreads();
+    };
+    for (int s = 0; s < steps; s += 2) {
+      step(A, B, s);
+      if (s + 1 < steps) step(B, A, s + 1);
+    }
+    l_run += __shfl_xor(l_run, 32);
+    // Half 1 leaves its state in LDS (every tile buffer is free after the
+    // last step's barrier); half 0 merges it into its own. Lane-interleaved
+    // 16-byte slots, so the stores and loads are free of bank conflicts.
+    float4* st = reinterpret_cast<float4*>(&bufs[1][0]);  // [w][4 NT][64 lanes]
+    float* ml = reinterpret_cast<float*>(&bufs[0][0]);    // m then l, [w][64 lanes] each
+    if (kh == 1) {
+#pragma unroll
+      for (int n = 0; n < NT; ++n)
+#pragma unroll
+        for (int r4 = 0; r4 < 4; ++r4)
+          st[(w * 4 * NT + 4 * n + r4) * 64 + lane] =
+              make_float4(acc[n][4 * r4], acc[n][4 * r4 + 1], acc[n][4 * r4 + 2], acc[n][4 * r4 + 3]);
+      ml[w * 64 + lane] = m_run;
+      ml[256 + w * 64 + lane] = l_run;
+    }
+    __syncthreads();
+    if (kh == 1) return;
+    const float m1 = ml[w * 64 + lane];
+    const float l1 = ml[256 + w * 64 + lane];
+    const float mn = fmaxf(m_run, m1);  // finite: half 0 holds key 0, visible to every row
+    const float a0 = fast_exp2((m_run - mn) * p.scale_log2);
+    const float a1 = m1 == -INFINITY ? 0.f : fast_exp2((m1 - mn) * p.scale_log2);
+#pragma unroll
+    for (int n = 0; n < NT; ++n)
+#pragma unroll
+      for (int r4 = 0; r4 < 4; ++r4) {
+        const float4 o1 = st[(w * 4 * NT + 4 * n + r4) * 64 + lane];
+        acc[n][4 * r4] = acc[n][4 * r4] * a0 + o1.x * a1;
+        acc[n][4 * r4 + 1] = acc[n][4 * r4 + 1] * a0 + o1.y * a1;
+        acc[n][4 * r4 + 2] = acc[n][4 * r4 + 2] * a0 + o1.z * a1;
+        acc[n][4 * r4 + 3] = acc[n][4 * r4 + 3] * a0 + o1.w * a1;
+      }
+    l_run = l_run * a0 + l1 * a1;
+    m_run = mn;
   }
-
-  l_run += __shfl_xor(l_run, 32);
   if (i >= M) return;
   const float inv = 1.f / l_run;
   const int64_t orow = (qs + i) * p.num_q_heads + qh;
@@ -442,19 +528,34 @@ __global__ __launch_bounds__(kPrefillThreads, 2) void prefill_mfma_kernel(const 
   if (h == 0 && p.lse != nullptr) p.lse[orow] = (m_run * p.scale_log2 + log2f(l_run)) * kLn2;
 }
 
+// Every form the host may launch, instantiated explicitly (clang emitted the
+// host launch stubs of only some of the instantiations referenced below).
+#define COMEM_PREFILL_FORMS(D, L) \
+  template __global__ void prefill_mfma_kernel<D, PLayout::L, 1>(const PrefillParams); \
+  template __global__ void prefill_mfma_kernel<D, PLayout::L, 2>(const PrefillParams);
+COMEM_PREFILL_FORMS(128, kContig)
+COMEM_PREFILL_FORMS(128, kPaged)
+COMEM_PREFILL_FORMS(128, kPagedFine)
+COMEM_PREFILL_FORMS(64, kContig)
+COMEM_PREFILL_FORMS(64, kPaged)
+COMEM_PREFILL_FORMS(64, kPagedFine)
+#undef COMEM_PREFILL_FORMS
+
 }  // namespace
 
-PrefillKernelFn select_prefill_kernel(int head_dim, int page_size) {
+template <int D, int KH>
+PrefillKernelFn prefill_by_layout(int page_size) {
   // page_size 0: contiguous cache. A paged cache takes the per-group path when
   // a group of a thread's rows (kPrefillThreads / (head_dim / 8) rows) fits in a page.
-  if (head_dim == 128) {
-    if (page_size == 0) return prefill_mfma_kernel<128, PLayout::kContig>;
-    return page_size >= 16 ? prefill_mfma_kernel<128, PLayout::kPaged> : prefill_mfma_kernel<128, PLayout::kPagedFine>;
-  }
-  if (head_dim == 64) {
-    if (page_size == 0) return prefill_mfma_kernel<64, PLayout::kContig>;
-    return page_size >= 32 ? prefill_mfma_kernel<64, PLayout::kPaged> : prefill_mfma_kernel<64, PLayout::kPagedFine>;
-  }
+  PrefillKernelFn fn = prefill_mfma_kernel<D, PLayout::kPagedFine, KH>;
+  if (page_size == 0) fn = prefill_mfma_kernel<D, PLayout::kContig, KH>;
+  else if (page_size >= 2048 / D) fn = prefill_mfma_kernel<D, PLayout::kPaged, KH>;
+  return fn;
+}
+
+PrefillKernelFn select_prefill_kernel(int head_dim, int page_size, bool key_split) {
+  if (head_dim == 128) return key_split ? prefill_by_layout<128, 2>(page_size) : prefill_by_layout<128, 1>(page_size);
+  if (head_dim == 64) return key_split ? prefill_by_layout<64, 2>(page_size) : prefill_by_layout<64, 1>(page_size);
   return nullptr;
 }
 

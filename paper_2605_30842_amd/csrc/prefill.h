@@ -38,7 +38,9 @@ struct PrefillParams {
 };
 
 using PrefillKernelFn = void (*)(PrefillParams);
-// page_size 0 selects the contiguous-cache kernel.
-PrefillKernelFn select_prefill_kernel(int head_dim, int page_size);
+// page_size 0 selects the contiguous-cache kernel. key_split: workgroups of
+// 8 waves, two per row group, each over half of the key tiles (for grids of
+// at most one workgroup per compute unit).
+PrefillKernelFn select_prefill_kernel(int head_dim, int page_size, bool key_split);
 
 }  // namespace comem
