@@ -55,6 +55,7 @@
 // the K reads (one chunk of 8 or 16 consecutive rows), the V transpose reads
 // (4 chunks of 4 consecutive rows) and the stores are all free of bank
 // conflicts. Paged caches look their block-table entries up one tile ahead.
+// (The 8-wave key-split form requests K two tiles and V one tile ahead.)
 #include "attn_common.h"
 #include "prefill.h"
 
@@ -97,6 +98,11 @@ __device__ inline int lds_offset(int r, int c) {
 enum class PLayout { kContig, kPaged, kPagedFine };
 
 typedef __attribute__((address_space(3))) void lds_void;
+
+// LDS byte address of a pointer into LDS (uniform: the caller's addresses are).
+__device__ inline uint32_t lds_address(char* p) {
+  return static_cast<uint32_t>(uniform_i32(static_cast<int>(reinterpret_cast<uintptr_t>((lds_void*)p))));
+}
 
 // Wave w loads rows 16 w .. 16 w + 15 of every K and V tile straight into
 // LDS (buffer loads with an LDS destination, no registers in between).
@@ -155,6 +161,70 @@ struct TileLoader {
     } else if constexpr (LAYOUT == PLayout::kPagedFine) {
 #pragma unroll
       for (int u = 0; u < NI; ++u) fine_page[u] = in_pool(bt_row[fine_key(t0, u) >> page_shift]);
+    }
+  }
+
+  // Page lookups of one tile, for the K and V loads of the ping-pong form,
+  // which load K two tiles ahead and V one tile ahead.
+  struct Pages {
+    int32_t page;
+    int32_t fine[NI];
+  };
+
+  __device__ Pages pages_of(int t0) const {
+    Pages pg{};
+    if constexpr (LAYOUT == PLayout::kPaged) {
+      const int g0 = t0 + 16 * w;
+      pg.page = g0 < kend ? in_pool(bt_row[g0 >> page_shift]) : 0;
+    } else if constexpr (LAYOUT == PLayout::kPagedFine) {
+#pragma unroll
+      for (int u = 0; u < NI; ++u) pg.fine[u] = in_pool(bt_row[fine_key(t0, u) >> page_shift]);
+    }
+    return pg;
+  }
+
+  // This wave's 16 rows of the K (or V) tile at key t0 into `dst`: NI loads.
+  // The loads are issued as inline assembly, invisible to the compiler's
+  // tracking of LDS writes by vector memory: the ping-pong loop orders them
+  // with its own waits and barriers, and the compiler's tracking (which
+  // confused the tile slots at the loop's head) would add waits of its own
+  // before the LDS reads of the other slots.
+  __device__ void load_rows(char* dst, const char* base, int t0, const Pages& pg) const {
+    constexpr int RB = D * 2;
+    char* d = dst + 16 * w * RB;
+    if constexpr (LAYOUT == PLayout::kPagedFine) {
+#pragma unroll
+      for (int u = 0; u < NI; ++u) {
+        const int t = fine_key(t0, u);
+        const int64_t off = static_cast<int64_t>(pg.fine[u]) * stride_page +
+                            static_cast<int64_t>(t & page_mask) * stride_token + 16 * ((lane % CH) ^ swizzle<D>(RPI * u + lane / CH));
+        const uint32_t lds = lds_address(d + u * RPI * RB);
+        asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, off" ::"s"(lds), "v"(base + off)
+                     : "memory", "m0");
+      }
+    } else {
+      const int g0 = t0 + 16 * w;
+      const int rows = max(0, min(kend - g0, 16));
+      int64_t off;
+      if constexpr (LAYOUT == PLayout::kContig) {
+        off = static_cast<int64_t>(g0) * stride_token;
+      } else {
+        off = static_cast<int64_t>(pg.page) * stride_page + static_cast<int64_t>(g0 & page_mask) * stride_token;
+      }
+      // Buffer descriptor (raw buffer: base, no stride, size in bytes, CDNA config word).
+      const uint64_t addr = reinterpret_cast<uint64_t>(base + off);
+      const int64_t bytes = static_cast<int64_t>(rows) * stride_token;
+      u32x4 r;
+      r[0] = static_cast<uint32_t>(addr);
+      r[1] = static_cast<uint32_t>(addr >> 32) & 0xffffu;
+      r[2] = bytes > 0xffffffffll ? 0xffffffffu : static_cast<uint32_t>(bytes);
+      r[3] = static_cast<uint32_t>(kBufferConfig);
+#pragma unroll
+      for (int u = 0; u < NI; ++u) {
+        const uint32_t lds = lds_address(d + u * RPI * RB);
+        asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds" ::"s"(lds), "v"(voff[u]), "s"(r)
+                     : "memory", "m0");
+      }
     }
   }
 
@@ -228,10 +298,10 @@ __device__ inline LaneOffsets<D> lane_offsets(int lane) {
   return o;
 }
 
-// One 64-key tile for the 32 rows of a wave. `limit` is the last key the
-// lane's row may see; MASKED is false when every key of the tile is visible
-// to every row of the workgroup.
-template <int D, bool MASKED, bool SAFE>
+// One 64-key tile for the 32 rows of a wave (the 4-wave form). `limit` is
+// the last key the lane's row may see; MASKED is false when every key of the
+// tile is visible to every row of the workgroup.
+template <int D, bool MASKED>
 __device__ inline void compute_tile(const TileBuf<D>& tb, int t0, int limit, int h, const LaneOffsets<D>& lo,
                                     const bf16x8 (&qop)[D / 16], float scale_log2, float& m_run, float& l_run,
                                     f32x16 (&acc)[D / 32]) {
@@ -272,21 +342,20 @@ __device__ inline void compute_tile(const TileBuf<D>& tb, int t0, int limit, int
   // Lazy maximum: move it only when some row would see a probability above
   // 2^kLazyMax. The first tile holds key 0, visible to every row, so the
   // maximum is finite from then on.
-  // With SAFE (the second half of a key-split workgroup, which starts in the
-  // middle of the keys) a row may have seen no key yet: its maximum is -inf,
-  // and its probabilities stay 0 until a visible key arrives.
   if (__builtin_amdgcn_ballot_w64((mt - m_run) * scale_log2 > kLazyMax) != 0) {
     const float m_new = fmaxf(m_run, mt);
-    float alpha = fast_exp2((m_run - m_new) * scale_log2);
-    if constexpr (SAFE) alpha = m_new == -INFINITY ? 1.f : alpha;
+    const float alpha = fast_exp2((m_run - m_new) * scale_log2);
 #pragma unroll
     for (int n = 0; n < NT; ++n) acc[n] *= alpha;
     l_run *= alpha;
     m_run = m_new;
   }
-  float mb = m_run * scale_log2;
-  if constexpr (SAFE) mb = m_run == -INFINITY ? 0.f : mb;
+  const float mb = m_run * scale_log2;
 
+  // The exponentials feed this wave's products step by step; a raised wave
+  // priority over that stretch lets the SIMD prefer it over the other
+  // workgroup's wave, whose score products then fill the gaps.
+  __builtin_amdgcn_s_setprio(1);
   float psum = 0.f;
 #pragma unroll
   for (int sb = 0; sb < 2; ++sb)
@@ -315,6 +384,138 @@ __device__ inline void compute_tile(const TileBuf<D>& tb, int t0, int limit, int
       }
     }
   l_run += psum;
+  __builtin_amdgcn_s_setprio(0);
+}
+
+// The ping-pong form splits the work of a tile into a matrix-core stage
+// (scores of this tile, products of the previous one) and a vector stage
+// (softmax of this tile), so that the two wave groups sharing the SIMDs can
+// run one stage each at the same time.
+template <int D>
+struct alignas(16) LdsTile {
+  char b[kPrefillTileKeys * D * 2];
+};
+
+// P^T operands of the four 16-key steps of a tile, hi and lo halves.
+struct PTile {
+  bf16x8 hi[2][2];
+  bf16x8 lo[2][2];
+};
+
+// S^T = K_tile . Q^T for the 32 rows of a wave.
+template <int D>
+__device__ inline void qk_scores(const char* kt, const LaneOffsets<D>& lo, const bf16x8 (&qop)[D / 16],
+                                 f32x16 (&s)[2]) {
+  constexpr int KS = D / 16;
+  constexpr int RB = D * 2;
+  s[0] = f32x16{};
+  s[1] = f32x16{};
+#pragma unroll
+  for (int ks = 0; ks < KS; ++ks) {
+    const int off = lo.k ^ (32 * ks);
+#pragma unroll
+    for (int sb = 0; sb < 2; ++sb) {
+      const bf16x8 kop = *reinterpret_cast<const bf16x8*>(kt + off + 32 * sb * RB);
+      s[sb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kop, qop[ks], s[sb], 0, 0, 0);
+    }
+  }
+}
+
+// Online softmax of one tile's scores: causal mask (when `masked`), lazy
+// maximum with rescaling of acc and l_run, probabilities split into P^T
+// operands, row sums into l_run. A row that has seen no visible key yet
+// keeps a maximum of -inf and zero probabilities.
+template <int D>
+__device__ inline void softmax_probs(f32x16 (&s)[2], bool masked, int t0, int limit, int h, float scale_log2,
+                                     float& m_run, float& l_run, f32x16 (&acc)[D / 32], PTile& pt) {
+  constexpr int NT = D / 32;
+  if (masked) {
+#pragma unroll
+    for (int sb = 0; sb < 2; ++sb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int t = t0 + 32 * sb + 8 * (r >> 2) + 4 * h + (r & 3);
+        if (t > limit) s[sb][r] = -INFINITY;
+      }
+  }
+  float mt = -INFINITY;
+#pragma unroll
+  for (int sb = 0; sb < 2; ++sb)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) mt = fmaxf(mt, s[sb][r]);
+  mt = fmaxf(mt, __shfl_xor(mt, 32));
+  if (__builtin_amdgcn_ballot_w64((mt - m_run) * scale_log2 > kLazyMax) != 0) {
+    const float m_new = fmaxf(m_run, mt);
+    float alpha = fast_exp2((m_run - m_new) * scale_log2);
+    alpha = m_new == -INFINITY ? 1.f : alpha;
+#pragma unroll
+    for (int n = 0; n < NT; ++n) acc[n] *= alpha;
+    l_run *= alpha;
+    m_run = m_new;
+  }
+  const float mb = m_run == -INFINITY ? 0.f : m_run * scale_log2;
+  float psum = 0.f;
+#pragma unroll
+  for (int sb = 0; sb < 2; ++sb)
+#pragma unroll
+    for (int s2 = 0; s2 < 2; ++s2) {
+      uint32_t ph[4], pl[4];
+#pragma unroll
+      for (int e = 0; e < 8; e += 2) {
+        const float p0 = fast_exp2(__builtin_fmaf(s[sb][8 * s2 + e], scale_log2, -mb));
+        const float p1 = fast_exp2(__builtin_fmaf(s[sb][8 * s2 + e + 1], scale_log2, -mb));
+        psum += p0 + p1;
+        split_bf16(p0, p1, ph[e >> 1], pl[e >> 1]);
+      }
+      pt.hi[sb][s2] = __builtin_bit_cast(bf16x8, u32x4{ph[0], ph[1], ph[2], ph[3]});
+      pt.lo[sb][s2] = __builtin_bit_cast(bf16x8, u32x4{pl[0], pl[1], pl[2], pl[3]});
+    }
+  l_run += psum;
+}
+
+// O^T += V_tile^T . P^T.
+template <int D>
+__device__ inline void pv_accumulate(const char* vt, const LaneOffsets<D>& lo, const PTile& pt, f32x16 (&acc)[D / 32]) {
+  constexpr int NT = D / 32;
+  constexpr int RB = D * 2;
+#pragma unroll
+  for (int sb = 0; sb < 2; ++sb)
+#pragma unroll
+    for (int s2 = 0; s2 < 2; ++s2) {
+      const int step = (32 * sb + 16 * s2) * RB;
+#pragma unroll
+      for (int n = 0; n < NT; ++n) {
+        const bf16x4 v0 = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(vt + step + (lo.v[0] ^ (64 * n))));
+        const bf16x4 v1 = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(vt + step + (lo.v[1] ^ (64 * n))));
+        const bf16x8 vop = __builtin_shufflevector(v0, v1, 0, 1, 2, 3, 4, 5, 6, 7);
+        acc[n] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vop, pt.hi[sb][s2], acc[n], 0, 0, 0);
+        acc[n] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vop, pt.lo[sb][s2], acc[n], 0, 0, 0);
+      }
+    }
+}
+
+// s_waitcnt immediate for vmcnt(n) with the other counters left alone (gfx9 encoding).
+constexpr int vmcnt_imm(int n) { return (n & 15) | ((n >> 4) << 14) | (7 << 4) | (15 << 8); }
+
+// Wait until at most N of this wave's vector memory requests are in flight,
+// at this point of the program (nothing is scheduled across it). The
+// compiler sees the wait, so it knows which tile requests have landed and
+// adds none of its own before the LDS reads.
+template <int N>
+__device__ inline void wait_vm() {
+  __builtin_amdgcn_sched_barrier(0);
+  __builtin_amdgcn_s_waitcnt(vmcnt_imm(N));
+  __builtin_amdgcn_sched_barrier(0);
+}
+
+// Workgroup barrier without the memory fence of __syncthreads, whose release
+// half would wait for every tile request in flight. The ping-pong loop writes
+// LDS only through those requests and orders them with wait_vm; each wave's
+// LDS reads have returned before its products use them.
+__device__ inline void stage_barrier() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
 }
 
 // Grid: (query blocks, KV heads, sequences); the kernel maps the workgroup
@@ -323,9 +524,10 @@ constexpr int kXcds = 8;  // XCDs of the GPU; workgroups are dealt to them round
 
 // KH = 2 (a key-split workgroup, for grids of at most one workgroup per
 // compute unit): waves 4..7 take the same 128 rows as waves 0..3 over the
-// second half of the key tiles, with their own pair of LDS buffers, so each
-// SIMD holds two waves as it would with two workgroups per compute unit. The
-// halves merge their softmax states through LDS at the end.
+// second half of the key tiles, with their own K and V slots, so each SIMD
+// holds one wave of each half. The halves run their tiles in ping-pong (one
+// half's products beside the other half's exponentials, see the loop) and
+// merge their softmax states through LDS at the end.
 template <int D, PLayout LAYOUT, int KH>
 __global__ __launch_bounds__(kPrefillThreads * KH, KH == 1 ? 2 : 1) void prefill_mfma_kernel(const PrefillParams p) {
   constexpr int KS = D / 16;
@@ -427,9 +629,9 @@ __global__ __launch_bounds__(kPrefillThreads * KH, KH == 1 ? 2 : 1) void prefill
         if (t + 2 < ntiles) ld.fetch_pages(kPrefillTileKeys * (t + 2));
       }
       if (t < nfree) {
-        compute_tile<D, false, false>(cur, kPrefillTileKeys * t, limit, h, lo, qop, p.scale_log2, m_run, l_run, acc);
+        compute_tile<D, false>(cur, kPrefillTileKeys * t, limit, h, lo, qop, p.scale_log2, m_run, l_run, acc);
       } else {
-        compute_tile<D, true, false>(cur, kPrefillTileKeys * t, limit, h, lo, qop, p.scale_log2, m_run, l_run, acc);
+        compute_tile<D, true>(cur, kPrefillTileKeys * t, limit, h, lo, qop, p.scale_log2, m_run, l_run, acc);
       }
       tile_loads_done();
       __syncthreads();
@@ -440,78 +642,132 @@ __global__ __launch_bounds__(kPrefillThreads * KH, KH == 1 ? 2 : 1) void prefill
     }
     l_run += __shfl_xor(l_run, 32);
   } else {
-    // Key half kh takes tiles [t_first, t_first + t_count) in `steps` steps
-    // (the same count in both halves, so that their barriers pair up), each
-    // half with its own pair of LDS buffers.
-    __shared__ TileBuf<D> bufs[2][2];
+    // Ping-pong key halves. Half kh (waves 4 kh .. 4 kh + 3, one per SIMD)
+    // takes tiles [t_first, t_first + t_count) with its own K and V slots.
+    // Its work is a chain of stages M(0) V(0) M(1) ... V(c-1) M(c), with
+    // M(i) the matrix-core stage (scores of tile i, products of tile i - 1)
+    // and V(i) the vector stage (softmax of tile i, which also requests V of
+    // tile i + 1 and K of tile i + 2). A barrier ends every stage, and half 1
+    // passes one extra barrier first, so it runs one stage behind half 0:
+    // while one half's waves issue products, the other half's waves on the
+    // same SIMDs compute exponentials. (A barrier counts arrivals, whatever
+    // instruction the waves reach it at.) Both halves pass the same number of
+    // barriers, with stages past their own tiles left empty.
+    // Slots: K of tile i in ks[i % 2], V of tile i in vs[i % 2], one entry
+    // per half.
+    __shared__ LdsTile<D> ks0[2], ks1[2], vs0[2], vs1[2];
+    using Pages = typename TileLoader<D, LAYOUT>::Pages;
     const int steps = (ntiles + 1) / 2;
     const int t_first = kh * steps;
-    const int t_count = min(steps, ntiles - t_first);
-    TileBuf<D>& A = bufs[kh][0];
-    TileBuf<D>& B = bufs[kh][1];
-    if (t_count > 0) {
-      ld.fetch_pages(kPrefillTileKeys * t_first);
-      ld.load(A, kPrefillTileKeys * t_first);
-      if (t_count > 1) ld.fetch_pages(kPrefillTileKeys * (t_first + 1));
+    const int t_count = max(0, min(steps, ntiles - t_first));
+    constexpr int TK = kPrefillTileKeys;
+    LdsTile<D>& k0 = ks0[kh];
+    LdsTile<D>& k1 = ks1[kh];
+    LdsTile<D>& v0 = vs0[kh];
+    LdsTile<D>& v1 = vs1[kh];
+    Pages pg_v, pg_k;  // page lookups of the next V and the next K tile to request
+    {
+      const Pages pg0 = ld.pages_of(TK * t_first);
+      const Pages pg1 = ld.pages_of(TK * (t_first + 1));
+      ld.load_rows(k0.b, ld.kbase, TK * t_first, pg0);
+      ld.load_rows(v0.b, ld.vbase, TK * t_first, pg0);
+      ld.load_rows(k1.b, ld.kbase, TK * (t_first + 1), pg1);
+      pg_v = pg1;
+      pg_k = ld.pages_of(TK * (t_first + 2));
     }
     load_q();
-    tile_loads_done();
+    wait_vm<0>();
     __syncthreads();
-    auto step = [&](const TileBuf<D>& cur, TileBuf<D>& nxt, int s) {
-      const int t = t_first + s;
-      if (s + 1 < t_count) {
-        ld.load(nxt, kPrefillTileKeys * (t + 1));
-        if (s + 2 < t_count) ld.fetch_pages(kPrefillTileKeys * (t + 2));
+
+    f32x16 s[2];  // scores of a tile between its M and V stages
+    PTile pt;     // probabilities of a tile between its V stage and the next M stage
+    auto m_stage = [&](const LdsTile<D>& kcur, const LdsTile<D>& vprev, int c) {
+      if (c >= 1 && c <= t_count) pv_accumulate<D>(vprev.b, lo, pt, acc);
+      if (c < t_count) qk_scores<D>(kcur.b, lo, qop, s);
+    };
+    // Every V stage requests two tiles (past the half's range they are
+    // unused; rows past the keys arrive as zeros), so the wait at its end
+    // leaves only its own requests in flight: those of the previous V stage,
+    // read in the next M stage, have landed. Both target slots were last read
+    // in the M stage just before.
+    constexpr int kStageLoads = 2 * TileLoader<D, LAYOUT>::NI;
+    auto v_stage = [&](LdsTile<D>& kslot, LdsTile<D>& vslot, int c) {
+      if (c < t_count) {
+        const int t = t_first + c;
+        ld.load_rows(vslot.b, ld.vbase, TK * (t + 1), pg_v);
+        ld.load_rows(kslot.b, ld.kbase, TK * (t + 2), pg_k);
+        pg_v = pg_k;
+        pg_k = ld.pages_of(TK * (t + 3));
+        softmax_probs<D>(s, t >= nfree, TK * t, limit, h, p.scale_log2, m_run, l_run, acc, pt);
+        wait_vm<kStageLoads>();
+      } else {
+        wait_vm<0>();  // so that the compiler knows nothing older is in flight on this path either
       }
-      if (s < t_count) {
-        if (t < nfree) {
-          compute_tile<D, false, true>(cur, kPrefillTileKeys * t, limit, h, lo, qop, p.scale_log2, m_run, l_run, acc);
+    };
+    if (kh == 1) stage_barrier();
+    for (int c = 0; c <= steps; c += 2) {
+      m_stage(k0, v1, c);
+      stage_barrier();
+      if (c < steps) {
+        v_stage(k0, v1, c);
+        stage_barrier();
+        m_stage(k1, v0, c + 1);
+        stage_barrier();
+        if (c + 1 < steps) {
+          v_stage(k1, v0, c + 1);
+          stage_barrier();
         } else {
-          compute_tile<D, true, true>(cur, kPrefillTileKeys * t, limit, h, lo, qop, p.scale_log2, m_run, l_run, acc);
+          wait_vm<0>();  // last pass: tells the compiler no request is in flight at the loop's head
         }
       }
-      tile_loads_done();
-      __syncthreads();
-    };
-    for (int s = 0; s < steps; s += 2) {
-      step(A, B, s);
-      if (s + 1 < steps) step(B, A, s + 1);
     }
+    if (kh == 0) stage_barrier();
     l_run += __shfl_xor(l_run, 32);
-    // Half 1 leaves its state in LDS (every tile buffer is free after the
-    // last step's barrier); half 0 merges it into its own. Lane-interleaved
-    // 16-byte slots, so the stores and loads are free of bank conflicts.
-    float4* st = reinterpret_cast<float4*>(&bufs[1][0]);  // [w][4 NT][64 lanes]
-    float* ml = reinterpret_cast<float*>(&bufs[0][0]);    // m then l, [w][64 lanes] each
+    // Half 1 leaves its state in LDS, once the last requests (unused tiles)
+    // have landed; half 0 merges it into its own, waves 0-1 then waves 2-3
+    // (each wave's accumulators take one 16 KB slot; lane-interleaved 16-byte
+    // stores and loads, free of bank conflicts). Every LDS access here names
+    // one variable, which keeps the variables' accesses in the loop apart for
+    // the compiler.
+    wait_vm<0>();
+    __syncthreads();
+    float* ml = reinterpret_cast<float*>(vs0[0].b);  // m then l, [w][64 lanes] each
     if (kh == 1) {
-#pragma unroll
-      for (int n = 0; n < NT; ++n)
-#pragma unroll
-        for (int r4 = 0; r4 < 4; ++r4)
-          st[(w * 4 * NT + 4 * n + r4) * 64 + lane] =
-              make_float4(acc[n][4 * r4], acc[n][4 * r4 + 1], acc[n][4 * r4 + 2], acc[n][4 * r4 + 3]);
       ml[w * 64 + lane] = m_run;
       ml[256 + w * 64 + lane] = l_run;
     }
-    __syncthreads();
-    if (kh == 1) return;
-    const float m1 = ml[w * 64 + lane];
-    const float l1 = ml[256 + w * 64 + lane];
-    const float mn = fmaxf(m_run, m1);  // finite: half 0 holds key 0, visible to every row
-    const float a0 = fast_exp2((m_run - mn) * p.scale_log2);
-    const float a1 = m1 == -INFINITY ? 0.f : fast_exp2((m1 - mn) * p.scale_log2);
+    for (int pass = 0; pass < 2; ++pass) {
+      float4* st = reinterpret_cast<float4*>(ks0[w & 1].b);  // [4 NT][64 lanes]
+      if (kh == 1 && (w >> 1) == pass) {
 #pragma unroll
-    for (int n = 0; n < NT; ++n)
+        for (int n = 0; n < NT; ++n)
 #pragma unroll
-      for (int r4 = 0; r4 < 4; ++r4) {
-        const float4 o1 = st[(w * 4 * NT + 4 * n + r4) * 64 + lane];
-        acc[n][4 * r4] = acc[n][4 * r4] * a0 + o1.x * a1;
-        acc[n][4 * r4 + 1] = acc[n][4 * r4 + 1] * a0 + o1.y * a1;
-        acc[n][4 * r4 + 2] = acc[n][4 * r4 + 2] * a0 + o1.z * a1;
-        acc[n][4 * r4 + 3] = acc[n][4 * r4 + 3] * a0 + o1.w * a1;
+          for (int r4 = 0; r4 < 4; ++r4)
+            st[(4 * n + r4) * 64 + lane] = make_float4(acc[n][4 * r4], acc[n][4 * r4 + 1], acc[n][4 * r4 + 2], acc[n][4 * r4 + 3]);
       }
-    l_run = l_run * a0 + l1 * a1;
-    m_run = mn;
+      __syncthreads();
+      if (kh == 0 && (w >> 1) == pass) {
+        const float m1 = ml[w * 64 + lane];
+        const float l1 = ml[256 + w * 64 + lane];
+        const float mn = fmaxf(m_run, m1);  // finite: half 0 holds key 0, visible to every row
+        const float a0 = fast_exp2((m_run - mn) * p.scale_log2);
+        const float a1 = m1 == -INFINITY ? 0.f : fast_exp2((m1 - mn) * p.scale_log2);
+#pragma unroll
+        for (int n = 0; n < NT; ++n)
+#pragma unroll
+          for (int r4 = 0; r4 < 4; ++r4) {
+            const float4 o1 = st[(4 * n + r4) * 64 + lane];
+            acc[n][4 * r4] = acc[n][4 * r4] * a0 + o1.x * a1;
+            acc[n][4 * r4 + 1] = acc[n][4 * r4 + 1] * a0 + o1.y * a1;
+            acc[n][4 * r4 + 2] = acc[n][4 * r4 + 2] * a0 + o1.z * a1;
+            acc[n][4 * r4 + 3] = acc[n][4 * r4 + 3] * a0 + o1.w * a1;
+          }
+        l_run = l_run * a0 + l1 * a1;
+        m_run = mn;
+      }
+      __syncthreads();
+    }
+    if (kh == 1) return;
   }
   if (i >= M) return;
   const float inv = 1.f / l_run;
