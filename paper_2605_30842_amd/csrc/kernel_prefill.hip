@@ -402,6 +402,23 @@ struct PTile {
   bf16x8 lo[2][2];
 };
 
+// Schedule N LDS reads and N products of a block so that the reads run A
+// ahead of the products (A reads first, then product and read alternating).
+template <int N, int A>
+__device__ inline void pipeline_reads() {
+  __builtin_amdgcn_sched_group_barrier(0x100, A, 0);
+#pragma unroll
+  for (int i = 0; i < N - A; ++i) {
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+    __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+  }
+  __builtin_amdgcn_sched_group_barrier(0x008, A, 0);
+}
+
+// Reads in flight ahead of the products: K reads in the score products, V
+// transpose reads in the output products (measured best of 2/4, 4/8, 6/8).
+constexpr int AHEAD_K = 6, AHEAD_V = 8;
+
 // S^T = K_tile . Q^T for the 32 rows of a wave.
 template <int D>
 __device__ inline void qk_scores(const char* kt, const LaneOffsets<D>& lo, const bf16x8 (&qop)[D / 16],
@@ -419,6 +436,7 @@ __device__ inline void qk_scores(const char* kt, const LaneOffsets<D>& lo, const
       s[sb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kop, qop[ks], s[sb], 0, 0, 0);
     }
   }
+  pipeline_reads<2 * KS, AHEAD_K>();
 }
 
 // Online softmax of one tile's scores: causal mask (when `masked`), lazy
@@ -492,6 +510,7 @@ __device__ inline void pv_accumulate(const char* vt, const LaneOffsets<D>& lo, c
         acc[n] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vop, pt.lo[sb][s2], acc[n], 0, 0, 0);
       }
     }
+  pipeline_reads<8 * NT, AHEAD_V>();
 }
 
 // s_waitcnt immediate for vmcnt(n) with the other counters left alone (gfx9 encoding).
