@@ -183,26 +183,28 @@ struct TileLoader {
     return pg;
   }
 
-  // This wave's 16 rows of the K (or V) tile at key t0 into `dst`: NI loads.
-  // The loads are issued as inline assembly, invisible to the compiler's
-  // tracking of LDS writes by vector memory: the ping-pong loop orders them
-  // with its own waits and barriers, and the compiler's tracking (which
-  // confused the tile slots at the loop's head) would add waits of its own
-  // before the LDS reads of the other slots.
-  __device__ void load_rows(char* dst, const char* base, int t0, const Pages& pg) const {
-    constexpr int RB = D * 2;
-    char* d = dst + 16 * w * RB;
-    if constexpr (LAYOUT == PLayout::kPagedFine) {
-#pragma unroll
-      for (int u = 0; u < NI; ++u) {
-        const int t = fine_key(t0, u);
-        const int64_t off = static_cast<int64_t>(pg.fine[u]) * stride_page +
-                            static_cast<int64_t>(t & page_mask) * stride_token + 16 * ((lane % CH) ^ swizzle<D>(RPI * u + lane / CH));
-        const uint32_t lds = lds_address(d + u * RPI * RB);
-        asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, off" ::"s"(lds), "v"(base + off)
-                     : "memory", "m0");
-      }
-    } else {
+  // Requests of the ping-pong form, issued as inline assembly: invisible to
+  // the compiler's tracking of LDS writes by vector memory, which confused
+  // the tile slots at the loop's head and added waits of its own before the
+  // LDS reads of the other slots. The loop orders the requests with its own
+  // waits and barriers.
+  //
+  // A tile request: this wave's 16 rows of the K (or V) tile at key t0.
+  // Contiguous and per-group paged layouts need one buffer descriptor per
+  // tile; pages under 16 rows per-lane addresses.
+  struct TileReq {
+    u32x4 rsrc;
+    const char* base;
+    int t0;
+    Pages pg;
+  };
+
+  __device__ TileReq tile_req(const char* base, int t0, const Pages& pg) const {
+    TileReq q;
+    q.base = base;
+    q.t0 = t0;
+    q.pg = pg;
+    if constexpr (LAYOUT != PLayout::kPagedFine) {
       const int g0 = t0 + 16 * w;
       const int rows = max(0, min(kend - g0, 16));
       int64_t off;
@@ -211,22 +213,37 @@ struct TileLoader {
       } else {
         off = static_cast<int64_t>(pg.page) * stride_page + static_cast<int64_t>(g0 & page_mask) * stride_token;
       }
-      // Buffer descriptor (raw buffer: base, no stride, size in bytes, CDNA config word).
+      // Raw buffer: base, no stride, size in bytes, CDNA config word.
       const uint64_t addr = reinterpret_cast<uint64_t>(base + off);
       const int64_t bytes = static_cast<int64_t>(rows) * stride_token;
-      u32x4 r;
-      r[0] = static_cast<uint32_t>(addr);
-      r[1] = static_cast<uint32_t>(addr >> 32) & 0xffffu;
-      r[2] = bytes > 0xffffffffll ? 0xffffffffu : static_cast<uint32_t>(bytes);
-      r[3] = static_cast<uint32_t>(kBufferConfig);
-#pragma unroll
-      for (int u = 0; u < NI; ++u) {
-        const uint32_t lds = lds_address(d + u * RPI * RB);
-        asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds" ::"s"(lds), "v"(voff[u]), "s"(r)
-                     : "memory", "m0");
-      }
+      q.rsrc[0] = static_cast<uint32_t>(addr);
+      q.rsrc[1] = static_cast<uint32_t>(addr >> 32) & 0xffffu;
+      q.rsrc[2] = bytes > 0xffffffffll ? 0xffffffffu : static_cast<uint32_t>(bytes);
+      q.rsrc[3] = static_cast<uint32_t>(kBufferConfig);
+    }
+    return q;
+  }
+
+  // Instruction u of a tile request (1 KiB of rows, u < NI) into LDS from
+  // lds_rows, the LDS address of this wave's first row of the slot.
+  __device__ void issue(const TileReq& q, uint32_t lds_rows, int u) const {
+    constexpr int RB = D * 2;
+    const uint32_t lds = lds_rows + u * RPI * RB;
+    if constexpr (LAYOUT == PLayout::kPagedFine) {
+      const int t = fine_key(q.t0, u);
+      const int64_t off = static_cast<int64_t>(q.pg.fine[u]) * stride_page + static_cast<int64_t>(t & page_mask) * stride_token +
+                          16 * ((lane % CH) ^ swizzle<D>(RPI * u + lane / CH));
+      asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, off" ::"s"(lds), "v"(q.base + off)
+                   : "memory", "m0");
+    } else {
+      asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds" ::"s"(lds), "v"(voff[u]),
+                   "s"(q.rsrc)
+                   : "memory", "m0");
     }
   }
+
+  // LDS address of this wave's first row in a tile slot.
+  __device__ uint32_t lds_rows(char* slot) const { return lds_address(slot + 16 * w * (D * 2)); }
 
   __device__ void load(TileBuf<D>& tb, int t0) const {
     constexpr int RB = D * 2;
@@ -443,9 +460,9 @@ __device__ inline void qk_scores(const char* kt, const LaneOffsets<D>& lo, const
 // maximum with rescaling of acc and l_run, probabilities split into P^T
 // operands, row sums into l_run. A row that has seen no visible key yet
 // keeps a maximum of -inf and zero probabilities.
-template <int D>
+template <int D, typename Hook>
 __device__ inline void softmax_probs(f32x16 (&s)[2], bool masked, int t0, int limit, int h, float scale_log2,
-                                     float& m_run, float& l_run, f32x16 (&acc)[D / 32], PTile& pt) {
+                                     float& m_run, float& l_run, f32x16 (&acc)[D / 32], PTile& pt, Hook&& hook) {
   constexpr int NT = D / 32;
   if (masked) {
 #pragma unroll
@@ -487,6 +504,12 @@ __device__ inline void softmax_probs(f32x16 (&s)[2], bool masked, int t0, int li
       }
       pt.hi[sb][s2] = __builtin_bit_cast(bf16x8, u32x4{ph[0], ph[1], ph[2], ph[3]});
       pt.lo[sb][s2] = __builtin_bit_cast(bf16x8, u32x4{pl[0], pl[1], pl[2], pl[3]});
+      // Work placed between the four parts of the exponentials (tile
+      // requests), kept there: requests issued back to back stall the wave
+      // while the address unit drains them.
+      __builtin_amdgcn_sched_barrier(0);
+      hook(2 * sb + s2);
+      __builtin_amdgcn_sched_barrier(0);
     }
   l_run += psum;
 }
@@ -684,13 +707,21 @@ __global__ __launch_bounds__(kPrefillThreads * KH, KH == 1 ? 2 : 1) void prefill
     LdsTile<D>& k1 = ks1[kh];
     LdsTile<D>& v0 = vs0[kh];
     LdsTile<D>& v1 = vs1[kh];
+    constexpr int NI = TileLoader<D, LAYOUT>::NI;
+    const uint32_t lk0 = ld.lds_rows(k0.b), lk1 = ld.lds_rows(k1.b), lv0 = ld.lds_rows(v0.b), lv1 = ld.lds_rows(v1.b);
     Pages pg_v, pg_k;  // page lookups of the next V and the next K tile to request
     {
       const Pages pg0 = ld.pages_of(TK * t_first);
       const Pages pg1 = ld.pages_of(TK * (t_first + 1));
-      ld.load_rows(k0.b, ld.kbase, TK * t_first, pg0);
-      ld.load_rows(v0.b, ld.vbase, TK * t_first, pg0);
-      ld.load_rows(k1.b, ld.kbase, TK * (t_first + 1), pg1);
+      const auto rk0 = ld.tile_req(ld.kbase, TK * t_first, pg0);
+      const auto rv0 = ld.tile_req(ld.vbase, TK * t_first, pg0);
+      const auto rk1 = ld.tile_req(ld.kbase, TK * (t_first + 1), pg1);
+#pragma unroll
+      for (int u = 0; u < NI; ++u) {
+        ld.issue(rk0, lk0, u);
+        ld.issue(rv0, lv0, u);
+        ld.issue(rk1, lk1, u);
+      }
       pg_v = pg1;
       pg_k = ld.pages_of(TK * (t_first + 2));
     }
@@ -710,14 +741,31 @@ __global__ __launch_bounds__(kPrefillThreads * KH, KH == 1 ? 2 : 1) void prefill
     // read in the next M stage, have landed. Both target slots were last read
     // in the M stage just before.
     constexpr int kStageLoads = 2 * TileLoader<D, LAYOUT>::NI;
-    auto v_stage = [&](LdsTile<D>& kslot, LdsTile<D>& vslot, int c) {
+    auto v_stage = [&](uint32_t kslot, uint32_t vslot, int c) {
       if (c < t_count) {
         const int t = t_first + c;
-        ld.load_rows(vslot.b, ld.vbase, TK * (t + 1), pg_v);
-        ld.load_rows(kslot.b, ld.kbase, TK * (t + 2), pg_k);
+        const auto rv = ld.tile_req(ld.vbase, TK * (t + 1), pg_v);
+        const auto rk = ld.tile_req(ld.kbase, TK * (t + 2), pg_k);
         pg_v = pg_k;
         pg_k = ld.pages_of(TK * (t + 3));
-        softmax_probs<D>(s, t >= nfree, TK * t, limit, h, p.scale_log2, m_run, l_run, acc, pt);
+        if constexpr (LAYOUT == PLayout::kPagedFine) {
+          // Per-lane addresses: issued at once rather than held in registers.
+#pragma unroll
+          for (int u = 0; u < NI; ++u) {
+            ld.issue(rv, vslot, u);
+            ld.issue(rk, kslot, u);
+          }
+          softmax_probs<D>(s, t >= nfree, TK * t, limit, h, p.scale_log2, m_run, l_run, acc, pt, [](int) {});
+        } else {
+          // Instructions spread over the four parts of the exponentials.
+          softmax_probs<D>(s, t >= nfree, TK * t, limit, h, p.scale_log2, m_run, l_run, acc, pt, [&](int part) {
+#pragma unroll
+            for (int u = part * NI / 4; u < (part + 1) * NI / 4; ++u) {
+              ld.issue(rv, vslot, u);
+              ld.issue(rk, kslot, u);
+            }
+          });
+        }
         wait_vm<kStageLoads>();
       } else {
         wait_vm<0>();  // so that the compiler knows nothing older is in flight on this path either
@@ -728,12 +776,12 @@ __global__ __launch_bounds__(kPrefillThreads * KH, KH == 1 ? 2 : 1) void prefill
       m_stage(k0, v1, c);
       stage_barrier();
       if (c < steps) {
-        v_stage(k0, v1, c);
+        v_stage(lk0, lv1, c);
         stage_barrier();
         m_stage(k1, v0, c + 1);
         stage_barrier();
         if (c + 1 < steps) {
-          v_stage(k1, v0, c + 1);
+          v_stage(lk1, lv0, c + 1);
           stage_barrier();
         } else {
           wait_vm<0>();  // last pass: tells the compiler no request is in flight at the loop's head
