@@ -96,7 +96,8 @@ def test_workgroup_forms(ps):
 
     assert workgroups(small) <= 256 < workgroups(big)
     for spec in (small, big):
-        _, _, _, out, lse, ro, rl, ra = _prefill_case(spec)
+        # Paged: spare pages poisoned with NaN, so a read outside the block table's pages would show.
+        _, _, _, out, lse, ro, rl, ra = _prefill_case(spec, **({"spare_pages": 3, "poison": True} if paged else {}))
         check_prefill(out, lse, ro, rl, ra, f"{f'paged ps={ps}' if paged else 'contiguous'} B={spec.kv.batch}")
 
 
