@@ -709,7 +709,7 @@ def _summary(r):
 def main():
     a = _args()
     if a.gpus != 1:
-        print(f"bench.py runs on one GPU only (asked for --gpus {a.gpus}); this build has no multi-GPU path.",
+        print(f"bench.py runs on one GPU only (asked for --gpus {a.gpus}); this library has no multi-GPU path.",
               file=sys.stderr)
         sys.exit(2)
     if a.steps < 1 or a.warmup < 0:
