@@ -540,9 +540,7 @@ __device__ inline void pv_accumulate(const char* vt, const LaneOffsets<D>& lo, c
 constexpr int vmcnt_imm(int n) { return (n & 15) | ((n >> 4) << 14) | (7 << 4) | (15 << 8); }
 
 // Wait until at most N of this wave's vector memory requests are in flight,
-// at this point of the program (nothing is scheduled across it). The
-// compiler sees the wait, so it knows which tile requests have landed and
-// adds none of its own before the LDS reads.
+// at this point of the program (nothing is scheduled across it).
 template <int N>
 __device__ inline void wait_vm() {
   __builtin_amdgcn_sched_barrier(0);
@@ -767,8 +765,6 @@ __global__ __launch_bounds__(kPrefillThreads * KH, KH == 1 ? 2 : 1) void prefill
           });
         }
         wait_vm<kStageLoads>();
-      } else {
-        wait_vm<0>();  // so that the compiler knows nothing older is in flight on this path either
       }
     };
     if (kh == 1) stage_barrier();
@@ -783,8 +779,6 @@ __global__ __launch_bounds__(kPrefillThreads * KH, KH == 1 ? 2 : 1) void prefill
         if (c + 1 < steps) {
           v_stage(lk1, lv0, c + 1);
           stage_barrier();
-        } else {
-          wait_vm<0>();  // last pass: tells the compiler no request is in flight at the loop's head
         }
       }
     }
@@ -793,9 +787,7 @@ __global__ __launch_bounds__(kPrefillThreads * KH, KH == 1 ? 2 : 1) void prefill
     // Half 1 leaves its state in LDS, once the last requests (unused tiles)
     // have landed; half 0 merges it into its own, waves 0-1 then waves 2-3
     // (each wave's accumulators take one 16 KB slot; lane-interleaved 16-byte
-    // stores and loads, free of bank conflicts). Every LDS access here names
-    // one variable, which keeps the variables' accesses in the loop apart for
-    // the compiler.
+    // stores and loads, free of bank conflicts).
     wait_vm<0>();
     __syncthreads();
     float* ml = reinterpret_cast<float*>(vs0[0].b);  // m then l, [w][64 lanes] each
