@@ -198,8 +198,6 @@ def _short_kernel_name(full):
         lay = re.search(r"Layout\)(\d)", a)
         if lay:
             name += "_" + ["contig", "paged", "pagedfine"][int(lay.group(1))]
-        elif a.isdigit() and base.startswith("prefill") and a in ("1", "2"):
-            name += "_keysplit" if a == "2" else ""  # workgroups of 8 waves over two key halves
         elif a.isdigit():
             name += f"_D{a}" if a in ("64", "128") else f"_{a}"
         elif "Bf16" in a:

@@ -58,12 +58,7 @@ comem_status prepare_prefill(const comem_decode_attn_plan& p, const void* q, con
 comem_status launch_prefill(const comem_decode_attn_plan& p, const comem::PrefillParams& a, bool paged,
                             int32_t batch, int32_t max_q_len, void* stream) {
   const int64_t blocks = ceil_div(max_q_len, a.tokens_per_block);
-  // With at most one 4-wave workgroup per compute unit, each SIMD would hold
-  // a single wave; workgroups of 8 waves that split the key tiles in two
-  // give each SIMD two.
-  const bool key_split = blocks * p.cfg.num_kv_heads * batch <= p.num_cus;
-  comem::PrefillKernelFn fn =
-      comem::select_prefill_kernel(p.cfg.head_dim, paged ? a.page_mask + 1 : 0, key_split);
+  comem::PrefillKernelFn fn = comem::select_prefill_kernel(p.cfg.head_dim, paged ? a.page_mask + 1 : 0);
   if (fn == nullptr) return COMEM_ERR_UNSUPPORTED;
   comem::PrefillParams args = a;
   void* argv[] = {&args};
@@ -71,7 +66,7 @@ comem_status launch_prefill(const comem_decode_attn_plan& p, const comem::Prefil
       hipLaunchKernel(reinterpret_cast<const void*>(fn),
                       dim3(static_cast<unsigned>(blocks), static_cast<unsigned>(p.cfg.num_kv_heads),
                            static_cast<unsigned>(batch)),
-                      dim3(comem::kPrefillThreads * (key_split ? 2 : 1)), argv, 0, static_cast<hipStream_t>(stream));
+                      dim3(comem::kPrefillThreads), argv, 0, static_cast<hipStream_t>(stream));
   return err == hipSuccess ? COMEM_OK : COMEM_ERR_HIP;
 }
 

@@ -9,8 +9,10 @@
 //
 // One workgroup takes 128 (new token, query head) rows of one KV head of one
 // sequence: 128 / G consecutive new tokens times the G query heads that share
-// the KV head, so every K/V tile staged in LDS serves all of them. Wave w
-// owns rows 32w .. 32w + 31 and, per 64-key tile, computes
+// the KV head, so every K/V tile staged in LDS serves all of them. It has 8
+// waves in two halves over the two halves of the key tiles (merged at the
+// end); wave w of a half owns rows 32w .. 32w + 31 and, per 64-key tile,
+// computes
 //   S^T[key, row] = K_tile . Q^T          (v_mfma_f32_32x32x16_bf16)
 //   O^T[d, row]  += V_tile^T . P^T        (same instruction)
 // with an online softmax in between. In the transposed form a lane owns one
@@ -47,15 +49,15 @@
 // rescaled rarely and every probability stays below 2^8.
 //
 // K and V tiles go from global memory straight into LDS (buffer loads with an
-// LDS destination), one tile ahead of the compute, into two LDS buffers. The
-// descriptors' base and size are uniform per 16-row group (one page when
-// pages hold 16 rows or more), so addresses are scalar arithmetic and rows
-// past the keys a block needs arrive as zeros. In
+// LDS destination), K two tiles and V one tile ahead of the compute, into two
+// K and two V slots per half. The descriptors' base and size are uniform per
+// 16-row group (one page when pages hold 16 rows or more), so addresses are
+// scalar arithmetic and rows past the keys a block needs arrive as zeros. In
 // LDS, 16-byte chunk c of row r sits at chunk c ^ f(r), with f chosen so that
 // the K reads (one chunk of 8 or 16 consecutive rows), the V transpose reads
 // (4 chunks of 4 consecutive rows) and the stores are all free of bank
-// conflicts. Paged caches look their block-table entries up one tile ahead.
-// (The 8-wave key-split form requests K two tiles and V one tile ahead.)
+// conflicts. Paged caches look their block-table entries up ahead of the
+// requests.
 #include "attn_common.h"
 #include "prefill.h"
 
@@ -72,27 +74,11 @@ typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
 
 constexpr float kLazyMax = 8.f;  // log2 of the largest probability the lazy maximum allows
 
-// One LDS buffer: a K tile and a V tile. The kernel keeps two as separate
-// objects, so the compiler can tell the loads streaming into one from the
-// reads of the other and does not wait for them.
-template <int D>
-struct TileBuf {
-  static constexpr int kTileBytes = kPrefillTileKeys * D * 2;
-  char k[kTileBytes];
-  char v[kTileBytes];
-};
-
 // Chunk swizzle of a row (depends on its low 4 bits only).
 template <int D>
 __device__ inline int swizzle(int r) {
   if constexpr (D == 128) return ((r & 3) << 2) | ((r >> 2) & 3);
   return (((r >> 1) & 1) << 2) | ((r >> 2) & 3);
-}
-
-// Byte offset of logical 16-byte chunk c of tile row r.
-template <int D>
-__device__ inline int lds_offset(int r, int c) {
-  return r * (D * 2) + ((c ^ swizzle<D>(r)) << 4);
 }
 
 enum class PLayout { kContig, kPaged, kPagedFine };
@@ -129,8 +115,6 @@ struct TileLoader {
   int kend;  // keys [0, kend) are needed
   int w, lane;
   uint32_t voff[NI];     // lane offset of instruction u within a 16-row group
-  int32_t page;          // kPaged: entry of this wave's group in the next tile to load (uniform)
-  int32_t fine_page[NI]; // kPagedFine: per-lane entries for the next tile to load
 
   __device__ void init(int wave, int ln) {
     w = wave;
@@ -142,30 +126,12 @@ struct TileLoader {
     }
   }
 
-  // Buffer descriptor over `rows` rows from `base`; never more than 4 GiB.
-  __device__ __amdgpu_buffer_rsrc_t rsrc(const char* base, int rows) const {
-    const int64_t bytes = static_cast<int64_t>(rows) * stride_token;
-    const uint32_t n = bytes > 0xffffffffll ? 0xffffffffu : static_cast<uint32_t>(bytes);
-    return __builtin_amdgcn_make_buffer_rsrc(const_cast<char*>(base), 0, static_cast<int>(n), kBufferConfig);
-  }
-
   __device__ int fine_key(int t0, int u) const { return min(t0 + 16 * w + RPI * u + lane / CH, kend - 1); }
 
   // A block-table entry outside the pool reads page 0.
   __device__ int32_t in_pool(int32_t page) const { return page < 0 || page >= num_pages ? 0 : page; }
 
-  __device__ void fetch_pages(int t0) {
-    if constexpr (LAYOUT == PLayout::kPaged) {
-      const int g0 = t0 + 16 * w;
-      page = g0 < kend ? in_pool(bt_row[g0 >> page_shift]) : 0;
-    } else if constexpr (LAYOUT == PLayout::kPagedFine) {
-#pragma unroll
-      for (int u = 0; u < NI; ++u) fine_page[u] = in_pool(bt_row[fine_key(t0, u) >> page_shift]);
-    }
-  }
-
-  // Page lookups of one tile, for the K and V loads of the ping-pong form,
-  // which load K two tiles ahead and V one tile ahead.
+  // Page lookups of one tile (K is requested two tiles ahead, V one).
   struct Pages {
     int32_t page;
     int32_t fine[NI];
@@ -183,7 +149,7 @@ struct TileLoader {
     return pg;
   }
 
-  // Requests of the ping-pong form, issued as inline assembly: invisible to
+  // Tile requests, issued as inline assembly: invisible to
   // the compiler's tracking of LDS writes by vector memory, which confused
   // the tile slots at the loop's head and added waits of its own before the
   // LDS reads of the other slots. The loop orders the requests with its own
@@ -245,41 +211,7 @@ struct TileLoader {
   // LDS address of this wave's first row in a tile slot.
   __device__ uint32_t lds_rows(char* slot) const { return lds_address(slot + 16 * w * (D * 2)); }
 
-  __device__ void load(TileBuf<D>& tb, int t0) const {
-    constexpr int RB = D * 2;
-    char* kd = tb.k + 16 * w * RB;
-    char* vd = tb.v + 16 * w * RB;
-    if constexpr (LAYOUT == PLayout::kPagedFine) {
-#pragma unroll
-      for (int u = 0; u < NI; ++u) {
-        const int t = fine_key(t0, u);
-        const int64_t off = static_cast<int64_t>(fine_page[u]) * stride_page +
-                            static_cast<int64_t>(t & page_mask) * stride_token + 16 * ((lane % CH) ^ swizzle<D>(RPI * u + lane / CH));
-        __builtin_amdgcn_global_load_lds(kbase + off, (lds_void*)(kd + u * RPI * RB), 16, 0, 0);
-        __builtin_amdgcn_global_load_lds(vbase + off, (lds_void*)(vd + u * RPI * RB), 16, 0, 0);
-      }
-    } else {
-      const int g0 = t0 + 16 * w;
-      const int rows = max(0, min(kend - g0, 16));
-      int64_t base;
-      if constexpr (LAYOUT == PLayout::kContig) {
-        base = static_cast<int64_t>(g0) * stride_token;
-      } else {
-        base = static_cast<int64_t>(page) * stride_page + static_cast<int64_t>(g0 & page_mask) * stride_token;
-      }
-      const __amdgpu_buffer_rsrc_t rk = rsrc(kbase + base, rows), rv = rsrc(vbase + base, rows);
-#pragma unroll
-      for (int u = 0; u < NI; ++u) {
-        __builtin_amdgcn_raw_ptr_buffer_load_lds(rk, (lds_void*)(kd + u * RPI * RB), 16, voff[u], 0, 0, 0);
-        __builtin_amdgcn_raw_ptr_buffer_load_lds(rv, (lds_void*)(vd + u * RPI * RB), 16, voff[u], 0, 0, 0);
-      }
-    }
-  }
 };
-
-// Tile loads land in LDS asynchronously: wait for this wave's, then the
-// barrier makes every wave's visible.
-__device__ inline void tile_loads_done() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
 
 // p0, p1 -> (hi, lo) bf16 pairs with p = hi + lo to about 2^-16 relative:
 // hi keeps the upper 16 bits of each value, lo is the exact fp32 remainder
@@ -315,96 +247,7 @@ __device__ inline LaneOffsets<D> lane_offsets(int lane) {
   return o;
 }
 
-// One 64-key tile for the 32 rows of a wave (the 4-wave form). `limit` is
-// the last key the lane's row may see; MASKED is false when every key of the
-// tile is visible to every row of the workgroup.
-template <int D, bool MASKED>
-__device__ inline void compute_tile(const TileBuf<D>& tb, int t0, int limit, int h, const LaneOffsets<D>& lo,
-                                    const bf16x8 (&qop)[D / 16], float scale_log2, float& m_run, float& l_run,
-                                    f32x16 (&acc)[D / 32]) {
-  constexpr int KS = D / 16;
-  constexpr int NT = D / 32;
-  constexpr int RB = D * 2;
-  const char* kt = tb.k;
-  const char* vt = tb.v;
-
-  // All K operands of the tile are read before the first product.
-  bf16x8 kop[KS][2];
-#pragma unroll
-  for (int ks = 0; ks < KS; ++ks) {
-    const int off = lo.k ^ (32 * ks);
-#pragma unroll
-    for (int sb = 0; sb < 2; ++sb) kop[ks][sb] = *reinterpret_cast<const bf16x8*>(kt + off + 32 * sb * RB);
-  }
-  f32x16 s[2] = {f32x16{}, f32x16{}};
-#pragma unroll
-  for (int ks = 0; ks < KS; ++ks)
-#pragma unroll
-    for (int sb = 0; sb < 2; ++sb) s[sb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kop[ks][sb], qop[ks], s[sb], 0, 0, 0);
-
-  // Raw scores keep their order (scale > 0), so the maximum is taken on them
-  // and the scale enters once, in the exponent.
-  float mt = -INFINITY;
-#pragma unroll
-  for (int sb = 0; sb < 2; ++sb)
-#pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      if constexpr (MASKED) {
-        const int t = t0 + 32 * sb + 8 * (r >> 2) + 4 * h + (r & 3);
-        if (t > limit) s[sb][r] = -INFINITY;
-      }
-      mt = fmaxf(mt, s[sb][r]);
-    }
-  mt = fmaxf(mt, __shfl_xor(mt, 32));
-  // Lazy maximum: move it only when some row would see a probability above
-  // 2^kLazyMax. The first tile holds key 0, visible to every row, so the
-  // maximum is finite from then on.
-  if (__builtin_amdgcn_ballot_w64((mt - m_run) * scale_log2 > kLazyMax) != 0) {
-    const float m_new = fmaxf(m_run, mt);
-    const float alpha = fast_exp2((m_run - m_new) * scale_log2);
-#pragma unroll
-    for (int n = 0; n < NT; ++n) acc[n] *= alpha;
-    l_run *= alpha;
-    m_run = m_new;
-  }
-  const float mb = m_run * scale_log2;
-
-  // The exponentials feed this wave's products step by step; a raised wave
-  // priority over that stretch lets the SIMD prefer it over the other
-  // workgroup's wave, whose score products then fill the gaps.
-  __builtin_amdgcn_s_setprio(1);
-  float psum = 0.f;
-#pragma unroll
-  for (int sb = 0; sb < 2; ++sb)
-#pragma unroll
-    for (int s2 = 0; s2 < 2; ++s2) {
-      uint32_t ph[4], pl[4];
-#pragma unroll
-      for (int e = 0; e < 8; e += 2) {
-        const float p0 = fast_exp2(__builtin_fmaf(s[sb][8 * s2 + e], scale_log2, -mb));
-        const float p1 = fast_exp2(__builtin_fmaf(s[sb][8 * s2 + e + 1], scale_log2, -mb));
-        psum += p0 + p1;
-        split_bf16(p0, p1, ph[e >> 1], pl[e >> 1]);
-      }
-      const bf16x8 pb_hi = __builtin_bit_cast(bf16x8, u32x4{ph[0], ph[1], ph[2], ph[3]});
-      const bf16x8 pb_lo = __builtin_bit_cast(bf16x8, u32x4{pl[0], pl[1], pl[2], pl[3]});
-      const int step = (32 * sb + 16 * s2) * RB;
-#pragma unroll
-      for (int n = 0; n < NT; ++n) {
-        const bf16x4 v0 = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
-            (lds_bf16x4*)(vt + step + (lo.v[0] ^ (64 * n))));
-        const bf16x4 v1 = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
-            (lds_bf16x4*)(vt + step + (lo.v[1] ^ (64 * n))));
-        const bf16x8 vop = __builtin_shufflevector(v0, v1, 0, 1, 2, 3, 4, 5, 6, 7);
-        acc[n] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vop, pb_hi, acc[n], 0, 0, 0);
-        acc[n] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vop, pb_lo, acc[n], 0, 0, 0);
-      }
-    }
-  l_run += psum;
-  __builtin_amdgcn_s_setprio(0);
-}
-
-// The ping-pong form splits the work of a tile into a matrix-core stage
+// The work of a tile is split into a matrix-core stage
 // (scores of this tile, products of the previous one) and a vector stage
 // (softmax of this tile), so that the two wave groups sharing the SIMDs can
 // run one stage each at the same time.
@@ -562,14 +405,14 @@ __device__ inline void stage_barrier() {
 // id to a work item itself (see the top of the kernel).
 constexpr int kXcds = 8;  // XCDs of the GPU; workgroups are dealt to them round robin
 
-// KH = 2 (a key-split workgroup, for grids of at most one workgroup per
-// compute unit): waves 4..7 take the same 128 rows as waves 0..3 over the
-// second half of the key tiles, with their own K and V slots, so each SIMD
-// holds one wave of each half. The halves run their tiles in ping-pong (one
-// half's products beside the other half's exponentials, see the loop) and
-// merge their softmax states through LDS at the end.
-template <int D, PLayout LAYOUT, int KH>
-__global__ __launch_bounds__(kPrefillThreads * KH, KH == 1 ? 2 : 1) void prefill_mfma_kernel(const PrefillParams p) {
+// One workgroup of 8 waves per block of 128 rows: waves 4..7 take the same
+// rows as waves 0..3 over the second half of the key tiles, with their own K
+// and V slots, so each SIMD holds one wave of each half. The halves run
+// their tiles in ping-pong (one half's products beside the other half's
+// exponentials, see the loop) and merge their softmax states through LDS at
+// the end.
+template <int D, PLayout LAYOUT>
+__global__ __launch_bounds__(kPrefillThreads, 1) void prefill_mfma_kernel(const PrefillParams p) {
   constexpr int KS = D / 16;
   constexpr int NT = D / 32;
   constexpr bool PAGED = LAYOUT != PLayout::kContig;
@@ -617,7 +460,7 @@ __global__ __launch_bounds__(kPrefillThreads * KH, KH == 1 ? 2 : 1) void prefill
   const int lane = threadIdx.x & 63;
   const int wv = uniform_i32(threadIdx.x >> 6);
   const int w = wv & 3;   // row group of the wave
-  const int kh = wv >> 2; // key half of the wave (0 unless KH = 2)
+  const int kh = wv >> 2; // key half of the wave
   const int j = lane & 31, h = lane >> 5;
   const int row = 32 * w + j;
   const int g = row / TB;
@@ -651,183 +494,151 @@ __global__ __launch_bounds__(kPrefillThreads * KH, KH == 1 ? 2 : 1) void prefill
   for (int n = 0; n < NT; ++n) acc[n] = f32x16{};
   float m_run = -INFINITY, l_run = 0.f;
 
-  if constexpr (KH == 1) {
-    __shared__ TileBuf<D> buf0, buf1;
-    ld.fetch_pages(0);
-    ld.load(buf0, 0);
-    if (ntiles > 1) ld.fetch_pages(kPrefillTileKeys);
-    load_q();
-    tile_loads_done();
-    __syncthreads();
-    // Tile t is in buffer t % 2 while tile t + 1 streams into the other one.
-    // Tiles before nfree are visible to every row whole; later ones take the
-    // causal mask. The loop handles two tiles per pass so that each half
-    // names its buffers statically.
-    auto step = [&](const TileBuf<D>& cur, TileBuf<D>& nxt, int t) {
-      if (t + 1 < ntiles) {
-        ld.load(nxt, kPrefillTileKeys * (t + 1));
-        if (t + 2 < ntiles) ld.fetch_pages(kPrefillTileKeys * (t + 2));
-      }
-      if (t < nfree) {
-        compute_tile<D, false>(cur, kPrefillTileKeys * t, limit, h, lo, qop, p.scale_log2, m_run, l_run, acc);
-      } else {
-        compute_tile<D, true>(cur, kPrefillTileKeys * t, limit, h, lo, qop, p.scale_log2, m_run, l_run, acc);
-      }
-      tile_loads_done();
-      __syncthreads();
-    };
-    for (int t = 0; t < ntiles; t += 2) {
-      step(buf0, buf1, t);
-      if (t + 1 < ntiles) step(buf1, buf0, t + 1);
-    }
-    l_run += __shfl_xor(l_run, 32);
-  } else {
-    // Ping-pong key halves. Half kh (waves 4 kh .. 4 kh + 3, one per SIMD)
-    // takes tiles [t_first, t_first + t_count) with its own K and V slots.
-    // Its work is a chain of stages M(0) V(0) M(1) ... V(c-1) M(c), with
-    // M(i) the matrix-core stage (scores of tile i, products of tile i - 1)
-    // and V(i) the vector stage (softmax of tile i, which also requests V of
-    // tile i + 1 and K of tile i + 2). A barrier ends every stage, and half 1
-    // passes one extra barrier first, so it runs one stage behind half 0:
-    // while one half's waves issue products, the other half's waves on the
-    // same SIMDs compute exponentials. (A barrier counts arrivals, whatever
-    // instruction the waves reach it at.) Both halves pass the same number of
-    // barriers, with stages past their own tiles left empty.
-    // Slots: K of tile i in ks[i % 2], V of tile i in vs[i % 2], one entry
-    // per half.
-    __shared__ LdsTile<D> ks0[2], ks1[2], vs0[2], vs1[2];
-    using Pages = typename TileLoader<D, LAYOUT>::Pages;
-    const int steps = (ntiles + 1) / 2;
-    const int t_first = kh * steps;
-    const int t_count = max(0, min(steps, ntiles - t_first));
-    constexpr int TK = kPrefillTileKeys;
-    LdsTile<D>& k0 = ks0[kh];
-    LdsTile<D>& k1 = ks1[kh];
-    LdsTile<D>& v0 = vs0[kh];
-    LdsTile<D>& v1 = vs1[kh];
-    constexpr int NI = TileLoader<D, LAYOUT>::NI;
-    const uint32_t lk0 = ld.lds_rows(k0.b), lk1 = ld.lds_rows(k1.b), lv0 = ld.lds_rows(v0.b), lv1 = ld.lds_rows(v1.b);
-    Pages pg_v, pg_k;  // page lookups of the next V and the next K tile to request
-    {
-      const Pages pg0 = ld.pages_of(TK * t_first);
-      const Pages pg1 = ld.pages_of(TK * (t_first + 1));
-      const auto rk0 = ld.tile_req(ld.kbase, TK * t_first, pg0);
-      const auto rv0 = ld.tile_req(ld.vbase, TK * t_first, pg0);
-      const auto rk1 = ld.tile_req(ld.kbase, TK * (t_first + 1), pg1);
+  // Ping-pong key halves. Half kh (waves 4 kh .. 4 kh + 3, one per SIMD)
+  // takes tiles [t_first, t_first + t_count) with its own K and V slots.
+  // Its work is a chain of stages M(0) V(0) M(1) ... V(c-1) M(c), with
+  // M(i) the matrix-core stage (scores of tile i, products of tile i - 1)
+  // and V(i) the vector stage (softmax of tile i, which also requests V of
+  // tile i + 1 and K of tile i + 2). A barrier ends every stage, and half 1
+  // passes one extra barrier first, so it runs one stage behind half 0:
+  // while one half's waves issue products, the other half's waves on the
+  // same SIMDs compute exponentials. (A barrier counts arrivals, whatever
+  // instruction the waves reach it at.) Both halves pass the same number of
+  // barriers, with stages past their own tiles left empty.
+  // Slots: K of tile i in ks[i % 2], V of tile i in vs[i % 2], one entry
+  // per half.
+  __shared__ LdsTile<D> ks0[2], ks1[2], vs0[2], vs1[2];
+  using Pages = typename TileLoader<D, LAYOUT>::Pages;
+  const int steps = (ntiles + 1) / 2;
+  const int t_first = kh * steps;
+  const int t_count = max(0, min(steps, ntiles - t_first));
+  constexpr int TK = kPrefillTileKeys;
+  LdsTile<D>& k0 = ks0[kh];
+  LdsTile<D>& k1 = ks1[kh];
+  LdsTile<D>& v0 = vs0[kh];
+  LdsTile<D>& v1 = vs1[kh];
+  constexpr int NI = TileLoader<D, LAYOUT>::NI;
+  const uint32_t lk0 = ld.lds_rows(k0.b), lk1 = ld.lds_rows(k1.b), lv0 = ld.lds_rows(v0.b), lv1 = ld.lds_rows(v1.b);
+  Pages pg_v, pg_k;  // page lookups of the next V and the next K tile to request
+  {
+    const Pages pg0 = ld.pages_of(TK * t_first);
+    const Pages pg1 = ld.pages_of(TK * (t_first + 1));
+    const auto rk0 = ld.tile_req(ld.kbase, TK * t_first, pg0);
+    const auto rv0 = ld.tile_req(ld.vbase, TK * t_first, pg0);
+    const auto rk1 = ld.tile_req(ld.kbase, TK * (t_first + 1), pg1);
 #pragma unroll
-      for (int u = 0; u < NI; ++u) {
-        ld.issue(rk0, lk0, u);
-        ld.issue(rv0, lv0, u);
-        ld.issue(rk1, lk1, u);
-      }
-      pg_v = pg1;
-      pg_k = ld.pages_of(TK * (t_first + 2));
+    for (int u = 0; u < NI; ++u) {
+      ld.issue(rk0, lk0, u);
+      ld.issue(rv0, lv0, u);
+      ld.issue(rk1, lk1, u);
     }
-    load_q();
-    wait_vm<0>();
-    __syncthreads();
+    pg_v = pg1;
+    pg_k = ld.pages_of(TK * (t_first + 2));
+  }
+  load_q();
+  wait_vm<0>();
+  __syncthreads();
 
-    f32x16 s[2];  // scores of a tile between its M and V stages
-    PTile pt;     // probabilities of a tile between its V stage and the next M stage
-    auto m_stage = [&](const LdsTile<D>& kcur, const LdsTile<D>& vprev, int c) {
-      if (c >= 1 && c <= t_count) pv_accumulate<D>(vprev.b, lo, pt, acc);
-      if (c < t_count) qk_scores<D>(kcur.b, lo, qop, s);
-    };
-    // Every V stage requests two tiles (past the half's range they are
-    // unused; rows past the keys arrive as zeros), so the wait at its end
-    // leaves only its own requests in flight: those of the previous V stage,
-    // read in the next M stage, have landed. Both target slots were last read
-    // in the M stage just before.
-    constexpr int kStageLoads = 2 * TileLoader<D, LAYOUT>::NI;
-    auto v_stage = [&](uint32_t kslot, uint32_t vslot, int c) {
-      if (c < t_count) {
-        const int t = t_first + c;
-        const auto rv = ld.tile_req(ld.vbase, TK * (t + 1), pg_v);
-        const auto rk = ld.tile_req(ld.kbase, TK * (t + 2), pg_k);
-        pg_v = pg_k;
-        pg_k = ld.pages_of(TK * (t + 3));
-        if constexpr (LAYOUT == PLayout::kPagedFine) {
-          // Per-lane addresses: issued at once rather than held in registers.
+  f32x16 s[2];  // scores of a tile between its M and V stages
+  PTile pt;     // probabilities of a tile between its V stage and the next M stage
+  auto m_stage = [&](const LdsTile<D>& kcur, const LdsTile<D>& vprev, int c) {
+    if (c >= 1 && c <= t_count) pv_accumulate<D>(vprev.b, lo, pt, acc);
+    if (c < t_count) qk_scores<D>(kcur.b, lo, qop, s);
+  };
+  // Every V stage requests two tiles (past the half's range they are
+  // unused; rows past the keys arrive as zeros), so the wait at its end
+  // leaves only its own requests in flight: those of the previous V stage,
+  // read in the next M stage, have landed. Both target slots were last read
+  // in the M stage just before.
+  constexpr int kStageLoads = 2 * TileLoader<D, LAYOUT>::NI;
+  auto v_stage = [&](uint32_t kslot, uint32_t vslot, int c) {
+    if (c < t_count) {
+      const int t = t_first + c;
+      const auto rv = ld.tile_req(ld.vbase, TK * (t + 1), pg_v);
+      const auto rk = ld.tile_req(ld.kbase, TK * (t + 2), pg_k);
+      pg_v = pg_k;
+      pg_k = ld.pages_of(TK * (t + 3));
+      if constexpr (LAYOUT == PLayout::kPagedFine) {
+        // Per-lane addresses: issued at once rather than held in registers.
 #pragma unroll
-          for (int u = 0; u < NI; ++u) {
+        for (int u = 0; u < NI; ++u) {
+          ld.issue(rv, vslot, u);
+          ld.issue(rk, kslot, u);
+        }
+        softmax_probs<D>(s, t >= nfree, TK * t, limit, h, p.scale_log2, m_run, l_run, acc, pt, [](int) {});
+      } else {
+        // Instructions spread over the four parts of the exponentials.
+        softmax_probs<D>(s, t >= nfree, TK * t, limit, h, p.scale_log2, m_run, l_run, acc, pt, [&](int part) {
+#pragma unroll
+          for (int u = part * NI / 4; u < (part + 1) * NI / 4; ++u) {
             ld.issue(rv, vslot, u);
             ld.issue(rk, kslot, u);
           }
-          softmax_probs<D>(s, t >= nfree, TK * t, limit, h, p.scale_log2, m_run, l_run, acc, pt, [](int) {});
-        } else {
-          // Instructions spread over the four parts of the exponentials.
-          softmax_probs<D>(s, t >= nfree, TK * t, limit, h, p.scale_log2, m_run, l_run, acc, pt, [&](int part) {
-#pragma unroll
-            for (int u = part * NI / 4; u < (part + 1) * NI / 4; ++u) {
-              ld.issue(rv, vslot, u);
-              ld.issue(rk, kslot, u);
-            }
-          });
-        }
-        wait_vm<kStageLoads>();
+        });
       }
-    };
-    if (kh == 1) stage_barrier();
-    for (int c = 0; c <= steps; c += 2) {
-      m_stage(k0, v1, c);
+      wait_vm<kStageLoads>();
+    }
+  };
+  if (kh == 1) stage_barrier();
+  for (int c = 0; c <= steps; c += 2) {
+    m_stage(k0, v1, c);
+    stage_barrier();
+    if (c < steps) {
+      v_stage(lk0, lv1, c);
       stage_barrier();
-      if (c < steps) {
-        v_stage(lk0, lv1, c);
+      m_stage(k1, v0, c + 1);
+      stage_barrier();
+      if (c + 1 < steps) {
+        v_stage(lk1, lv0, c + 1);
         stage_barrier();
-        m_stage(k1, v0, c + 1);
-        stage_barrier();
-        if (c + 1 < steps) {
-          v_stage(lk1, lv0, c + 1);
-          stage_barrier();
-        }
       }
     }
-    if (kh == 0) stage_barrier();
-    l_run += __shfl_xor(l_run, 32);
-    // Half 1 leaves its state in LDS, once the last requests (unused tiles)
-    // have landed; half 0 merges it into its own, waves 0-1 then waves 2-3
-    // (each wave's accumulators take one 16 KB slot; lane-interleaved 16-byte
-    // stores and loads, free of bank conflicts).
-    wait_vm<0>();
-    __syncthreads();
-    float* ml = reinterpret_cast<float*>(vs0[0].b);  // m then l, [w][64 lanes] each
-    if (kh == 1) {
-      ml[w * 64 + lane] = m_run;
-      ml[256 + w * 64 + lane] = l_run;
-    }
-    for (int pass = 0; pass < 2; ++pass) {
-      float4* st = reinterpret_cast<float4*>(ks0[w & 1].b);  // [4 NT][64 lanes]
-      if (kh == 1 && (w >> 1) == pass) {
-#pragma unroll
-        for (int n = 0; n < NT; ++n)
-#pragma unroll
-          for (int r4 = 0; r4 < 4; ++r4)
-            st[(4 * n + r4) * 64 + lane] = make_float4(acc[n][4 * r4], acc[n][4 * r4 + 1], acc[n][4 * r4 + 2], acc[n][4 * r4 + 3]);
-      }
-      __syncthreads();
-      if (kh == 0 && (w >> 1) == pass) {
-        const float m1 = ml[w * 64 + lane];
-        const float l1 = ml[256 + w * 64 + lane];
-        const float mn = fmaxf(m_run, m1);  // finite: half 0 holds key 0, visible to every row
-        const float a0 = fast_exp2((m_run - mn) * p.scale_log2);
-        const float a1 = m1 == -INFINITY ? 0.f : fast_exp2((m1 - mn) * p.scale_log2);
-#pragma unroll
-        for (int n = 0; n < NT; ++n)
-#pragma unroll
-          for (int r4 = 0; r4 < 4; ++r4) {
-            const float4 o1 = st[(4 * n + r4) * 64 + lane];
-            acc[n][4 * r4] = acc[n][4 * r4] * a0 + o1.x * a1;
-            acc[n][4 * r4 + 1] = acc[n][4 * r4 + 1] * a0 + o1.y * a1;
-            acc[n][4 * r4 + 2] = acc[n][4 * r4 + 2] * a0 + o1.z * a1;
-            acc[n][4 * r4 + 3] = acc[n][4 * r4 + 3] * a0 + o1.w * a1;
-          }
-        l_run = l_run * a0 + l1 * a1;
-        m_run = mn;
-      }
-      __syncthreads();
-    }
-    if (kh == 1) return;
   }
+  if (kh == 0) stage_barrier();
+  l_run += __shfl_xor(l_run, 32);
+  // Half 1 leaves its state in LDS, once the last requests (unused tiles)
+  // have landed; half 0 merges it into its own, waves 0-1 then waves 2-3
+  // (each wave's accumulators take one 16 KB slot; lane-interleaved 16-byte
+  // stores and loads, free of bank conflicts).
+  wait_vm<0>();
+  __syncthreads();
+  float* ml = reinterpret_cast<float*>(vs0[0].b);  // m then l, [w][64 lanes] each
+  if (kh == 1) {
+    ml[w * 64 + lane] = m_run;
+    ml[256 + w * 64 + lane] = l_run;
+  }
+  for (int pass = 0; pass < 2; ++pass) {
+    float4* st = reinterpret_cast<float4*>(ks0[w & 1].b);  // [4 NT][64 lanes]
+    if (kh == 1 && (w >> 1) == pass) {
+#pragma unroll
+      for (int n = 0; n < NT; ++n)
+#pragma unroll
+        for (int r4 = 0; r4 < 4; ++r4)
+          st[(4 * n + r4) * 64 + lane] = make_float4(acc[n][4 * r4], acc[n][4 * r4 + 1], acc[n][4 * r4 + 2], acc[n][4 * r4 + 3]);
+    }
+    __syncthreads();
+    if (kh == 0 && (w >> 1) == pass) {
+      const float m1 = ml[w * 64 + lane];
+      const float l1 = ml[256 + w * 64 + lane];
+      const float mn = fmaxf(m_run, m1);  // finite: half 0 holds key 0, visible to every row
+      const float a0 = fast_exp2((m_run - mn) * p.scale_log2);
+      const float a1 = m1 == -INFINITY ? 0.f : fast_exp2((m1 - mn) * p.scale_log2);
+#pragma unroll
+      for (int n = 0; n < NT; ++n)
+#pragma unroll
+        for (int r4 = 0; r4 < 4; ++r4) {
+          const float4 o1 = st[(4 * n + r4) * 64 + lane];
+          acc[n][4 * r4] = acc[n][4 * r4] * a0 + o1.x * a1;
+          acc[n][4 * r4 + 1] = acc[n][4 * r4 + 1] * a0 + o1.y * a1;
+          acc[n][4 * r4 + 2] = acc[n][4 * r4 + 2] * a0 + o1.z * a1;
+          acc[n][4 * r4 + 3] = acc[n][4 * r4 + 3] * a0 + o1.w * a1;
+        }
+      l_run = l_run * a0 + l1 * a1;
+      m_run = mn;
+    }
+    __syncthreads();
+  }
+  if (kh == 1) return;
   if (i >= M) return;
   const float inv = 1.f / l_run;
   const int64_t orow = (qs + i) * p.num_q_heads + qh;
@@ -845,9 +656,7 @@ __global__ __launch_bounds__(kPrefillThreads * KH, KH == 1 ? 2 : 1) void prefill
 
 // Every form the host may launch, instantiated explicitly (clang emitted the
 // host launch stubs of only some of the instantiations referenced below).
-#define COMEM_PREFILL_FORMS(D, L) \
-  template __global__ void prefill_mfma_kernel<D, PLayout::L, 1>(const PrefillParams); \
-  template __global__ void prefill_mfma_kernel<D, PLayout::L, 2>(const PrefillParams);
+#define COMEM_PREFILL_FORMS(D, L) template __global__ void prefill_mfma_kernel<D, PLayout::L>(const PrefillParams);
 COMEM_PREFILL_FORMS(128, kContig)
 COMEM_PREFILL_FORMS(128, kPaged)
 COMEM_PREFILL_FORMS(128, kPagedFine)
@@ -858,19 +667,19 @@ COMEM_PREFILL_FORMS(64, kPagedFine)
 
 }  // namespace
 
-template <int D, int KH>
+template <int D>
 PrefillKernelFn prefill_by_layout(int page_size) {
   // page_size 0: contiguous cache. A paged cache takes the per-group path when
-  // a group of a thread's rows (kPrefillThreads / (head_dim / 8) rows) fits in a page.
-  PrefillKernelFn fn = prefill_mfma_kernel<D, PLayout::kPagedFine, KH>;
-  if (page_size == 0) fn = prefill_mfma_kernel<D, PLayout::kContig, KH>;
-  else if (page_size >= 2048 / D) fn = prefill_mfma_kernel<D, PLayout::kPaged, KH>;
+  // a wave's 16-row group of a tile fits in a page.
+  PrefillKernelFn fn = prefill_mfma_kernel<D, PLayout::kPagedFine>;
+  if (page_size == 0) fn = prefill_mfma_kernel<D, PLayout::kContig>;
+  else if (page_size >= 2048 / D) fn = prefill_mfma_kernel<D, PLayout::kPaged>;
   return fn;
 }
 
-PrefillKernelFn select_prefill_kernel(int head_dim, int page_size, bool key_split) {
-  if (head_dim == 128) return key_split ? prefill_by_layout<128, 2>(page_size) : prefill_by_layout<128, 1>(page_size);
-  if (head_dim == 64) return key_split ? prefill_by_layout<64, 2>(page_size) : prefill_by_layout<64, 1>(page_size);
+PrefillKernelFn select_prefill_kernel(int head_dim, int page_size) {
+  if (head_dim == 128) return prefill_by_layout<128>(page_size);
+  if (head_dim == 64) return prefill_by_layout<64>(page_size);
   return nullptr;
 }
 

@@ -6,7 +6,7 @@
 
 namespace comem {
 
-constexpr int kPrefillThreads = 256;  // 4 waves
+constexpr int kPrefillThreads = 512;  // 8 waves: two halves of the key tiles, 4 waves each
 constexpr int kPrefillRows = 128;     // (query token, query head) rows per workgroup: 32 per wave
 constexpr int kPrefillTileKeys = 64;  // keys per K/V tile staged in LDS
 
@@ -38,9 +38,7 @@ struct PrefillParams {
 };
 
 using PrefillKernelFn = void (*)(PrefillParams);
-// page_size 0 selects the contiguous-cache kernel. key_split: workgroups of
-// 8 waves, two per row group, each over half of the key tiles (for grids of
-// at most one workgroup per compute unit).
-PrefillKernelFn select_prefill_kernel(int head_dim, int page_size, bool key_split);
+// page_size 0 selects the contiguous-cache kernel.
+PrefillKernelFn select_prefill_kernel(int head_dim, int page_size);
 
 }  // namespace comem

@@ -74,12 +74,13 @@ def test_paged_with_poison(ps):
 
 
 @pytest.mark.parametrize("ps", [0, 16, 8, 1])
-def test_workgroup_forms(ps):
-    """Grids of at most one 4-wave workgroup per compute unit take workgroups of 8 waves that split the key
-    tiles in two; larger grids take 4-wave workgroups. The same sequences (uncached, long-prefix, one-tile and
-    odd tile counts) run in both forms: alone (6 sequences, 240 workgroups) and inside a batch of 48 (one
-    workgroup per sequence and KV head, over 256 workgroups), and both match the oracle. ps: 0 for the
-    contiguous cache, else the page size (pages of 8 and 1 tokens take per-lane addresses)."""
+def test_grid_sizes(ps):
+    """The same sequences (uncached, long-prefix, one-tile and odd tile counts) in a grid that fits the
+    compute units at once (6 sequences, 240 workgroups) and inside a batch of 48 (one workgroup per
+    sequence and KV head, over 256 workgroups, which the GPU runs in turns) match the oracle. Both halves
+    of each workgroup's key tiles see every kind of tile: the first, a masked last one, one past the
+    keys. ps: 0 for the contiguous cache, else the page size (pages of 8 and 1 tokens take per-lane
+    addresses)."""
     paged = ps > 0
     lens = [1, 64, 65, 700, 300, 129]
     news = [1, 64, 33, 31, 150, 2]
@@ -91,7 +92,7 @@ def test_workgroup_forms(ps):
     big_l = lens + [int(x) for x in r.integers(1, 400, size=42)]
     big_m = news + [int(min(L, m)) for L, m in zip(big_l[len(lens):], r.integers(1, 33, size=42))]
     big = with_pages(small_prefill_spec(base, big_l, big_m, seed=58, **({"max_ctx_len": 704} if paged else {})))
-    def workgroups(spec):  # grid of the 4-wave form: blocks of 128 / G new tokens x KV heads x sequences
+    def workgroups(spec):  # grid: blocks of 128 / G new tokens x KV heads x sequences
         return -(-max(spec.new_tokens[1]) // (128 // spec.kv.group)) * spec.kv.num_kv_heads * spec.kv.batch
 
     assert workgroups(small) <= 256 < workgroups(big)
