@@ -72,7 +72,8 @@ typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
 
-constexpr float kLazyMax = 8.f;  // log2 of the largest probability the lazy maximum allows
+constexpr float kLazyMax = 8.f;        // log2 of the largest probability the lazy maximum allows
+constexpr float kLazyMaxProb = 256.f;  // 2^kLazyMax
 
 // Chunk swizzle of a row (depends on its low 4 bits only).
 template <int D>
@@ -137,11 +138,16 @@ struct TileLoader {
     int32_t fine[NI];
   };
 
+  // The per-group lookup reads the block table (not written during the call)
+  // through the constant address space, so it becomes a scalar load. As a
+  // vector load it came with a wait for every vector memory request in
+  // flight, the tile requests included, in every vector stage.
   __device__ Pages pages_of(int t0) const {
     Pages pg{};
     if constexpr (LAYOUT == PLayout::kPaged) {
+      typedef const __attribute__((address_space(4))) int32_t* ConstI32;
       const int g0 = t0 + 16 * w;
-      pg.page = g0 < kend ? in_pool(bt_row[g0 >> page_shift]) : 0;
+      pg.page = g0 < kend ? in_pool(((ConstI32)bt_row)[g0 >> page_shift]) : 0;
     } else if constexpr (LAYOUT == PLayout::kPagedFine) {
 #pragma unroll
       for (int u = 0; u < NI; ++u) pg.fine[u] = in_pool(bt_row[fine_key(t0, u) >> page_shift]);
@@ -191,7 +197,10 @@ struct TileLoader {
   }
 
   // Instruction u of a tile request (1 KiB of rows, u < NI) into LDS from
-  // lds_rows, the LDS address of this wave's first row of the slot.
+  // lds_rows, the LDS address of this wave's first row of the slot. The
+  // LDS address goes in m0, an operand of the asm, so the compiler writes
+  // m0 itself; the s_nop covers the wait state an LDS-bound load needs after
+  // an m0 write.
   __device__ void issue(const TileReq& q, uint32_t lds_rows, int u) const {
     constexpr int RB = D * 2;
     const uint32_t lds = lds_rows + u * RPI * RB;
@@ -199,12 +208,10 @@ struct TileLoader {
       const int t = fine_key(q.t0, u);
       const int64_t off = static_cast<int64_t>(q.pg.fine[u]) * stride_page + static_cast<int64_t>(t & page_mask) * stride_token +
                           16 * ((lane % CH) ^ swizzle<D>(RPI * u + lane / CH));
-      asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, off" ::"s"(lds), "v"(q.base + off)
-                   : "memory", "m0");
+      asm volatile("s_nop 0\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(q.base + off), "{m0}"(lds) : "memory");
     } else {
-      asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds" ::"s"(lds), "v"(voff[u]),
-                   "s"(q.rsrc)
-                   : "memory", "m0");
+      asm volatile("s_nop 0\n\tbuffer_load_dwordx4 %0, %1, 0 offen lds" ::"v"(voff[u]), "s"(q.rsrc), "{m0}"(lds)
+                   : "memory");
     }
   }
 
@@ -299,40 +306,13 @@ __device__ inline void qk_scores(const char* kt, const LaneOffsets<D>& lo, const
   pipeline_reads<2 * KS, AHEAD_K>();
 }
 
-// Online softmax of one tile's scores: causal mask (when `masked`), lazy
-// maximum with rescaling of acc and l_run, probabilities split into P^T
-// operands, row sums into l_run. A row that has seen no visible key yet
-// keeps a maximum of -inf and zero probabilities.
-template <int D, typename Hook>
-__device__ inline void softmax_probs(f32x16 (&s)[2], bool masked, int t0, int limit, int h, float scale_log2,
-                                     float& m_run, float& l_run, f32x16 (&acc)[D / 32], PTile& pt, Hook&& hook) {
-  constexpr int NT = D / 32;
-  if (masked) {
-#pragma unroll
-    for (int sb = 0; sb < 2; ++sb)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int t = t0 + 32 * sb + 8 * (r >> 2) + 4 * h + (r & 3);
-        if (t > limit) s[sb][r] = -INFINITY;
-      }
-  }
-  float mt = -INFINITY;
-#pragma unroll
-  for (int sb = 0; sb < 2; ++sb)
-#pragma unroll
-    for (int r = 0; r < 16; ++r) mt = fmaxf(mt, s[sb][r]);
-  mt = fmaxf(mt, __shfl_xor(mt, 32));
-  if (__builtin_amdgcn_ballot_w64((mt - m_run) * scale_log2 > kLazyMax) != 0) {
-    const float m_new = fmaxf(m_run, mt);
-    float alpha = fast_exp2((m_run - m_new) * scale_log2);
-    alpha = m_new == -INFINITY ? 1.f : alpha;
-#pragma unroll
-    for (int n = 0; n < NT; ++n) acc[n] *= alpha;
-    l_run *= alpha;
-    m_run = m_new;
-  }
-  const float mb = m_run == -INFINITY ? 0.f : m_run * scale_log2;
-  float psum = 0.f;
+// Probabilities of one tile's scores against the reference exponent mb
+// (the running maximum times scale_log2), split into P^T operands; the row's
+// sum goes to psum. hook(part) runs after each quarter of the exponentials
+// (tile requests placed there, kept there: requests issued back to back
+// stall the wave while the address unit drains them).
+template <typename Hook>
+__device__ inline void probs_at(const f32x16 (&s)[2], float mb, float scale_log2, float& psum, PTile& pt, Hook&& hook) {
 #pragma unroll
   for (int sb = 0; sb < 2; ++sb)
 #pragma unroll
@@ -347,13 +327,62 @@ __device__ inline void softmax_probs(f32x16 (&s)[2], bool masked, int t0, int li
       }
       pt.hi[sb][s2] = __builtin_bit_cast(bf16x8, u32x4{ph[0], ph[1], ph[2], ph[3]});
       pt.lo[sb][s2] = __builtin_bit_cast(bf16x8, u32x4{pl[0], pl[1], pl[2], pl[3]});
-      // Work placed between the four parts of the exponentials (tile
-      // requests), kept there: requests issued back to back stall the wave
-      // while the address unit drains them.
       __builtin_amdgcn_sched_barrier(0);
       hook(2 * sb + s2);
       __builtin_amdgcn_sched_barrier(0);
     }
+}
+
+// Online softmax of one tile's scores: causal mask (when `masked`), lazy
+// maximum with rescaling of acc and l_run, probabilities split into P^T
+// operands, row sums into l_run. A row that has seen no visible key yet
+// keeps a maximum of -inf and zero probabilities.
+//
+// The probabilities are first taken against the running maximum as it is.
+// Each is at most the sum a lane takes of them, so sums of at most 2^8 in
+// every lane show that no probability exceeds what the lazy maximum allows,
+// and they are kept. Otherwise (or with a row that has no maximum yet) the
+// whole wave takes the tile's maximum, rescales where the lazy-maximum rule
+// says so and takes the probabilities again, the same steps as without the
+// first try. The common case so skips the maximum (32 comparisons, a
+// shuffle and a vote per lane).
+template <int D, typename Hook>
+__device__ inline void softmax_probs(f32x16 (&s)[2], bool masked, int t0, int limit, int h, float scale_log2,
+                                     float& m_run, float& l_run, f32x16 (&acc)[D / 32], PTile& pt, Hook&& hook) {
+  constexpr int NT = D / 32;
+  if (masked) {
+#pragma unroll
+    for (int sb = 0; sb < 2; ++sb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int t = t0 + 32 * sb + 8 * (r >> 2) + 4 * h + (r & 3);
+        if (t > limit) s[sb][r] = -INFINITY;
+      }
+  }
+  // The first try runs in every wave (its hook issues the tile requests).
+  float psum = 0.f;
+  probs_at(s, m_run == -INFINITY ? 0.f : m_run * scale_log2, scale_log2, psum, pt, hook);
+  const bool redo = m_run == -INFINITY || !(psum <= kLazyMaxProb);
+  if (__builtin_amdgcn_ballot_w64(redo) != 0) {
+    float mt = -INFINITY;
+#pragma unroll
+    for (int sb = 0; sb < 2; ++sb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) mt = fmaxf(mt, s[sb][r]);
+    mt = fmaxf(mt, __shfl_xor(mt, 32));
+    if (__builtin_amdgcn_ballot_w64((mt - m_run) * scale_log2 > kLazyMax) != 0) {
+      const float m_new = fmaxf(m_run, mt);
+      float alpha = fast_exp2((m_run - m_new) * scale_log2);
+      alpha = m_new == -INFINITY ? 1.f : alpha;
+#pragma unroll
+      for (int n = 0; n < NT; ++n) acc[n] *= alpha;
+      l_run *= alpha;
+      m_run = m_new;
+    }
+    const float mb = m_run == -INFINITY ? 0.f : m_run * scale_log2;
+    psum = 0.f;
+    probs_at(s, mb, scale_log2, psum, pt, [](int) {});
+  }
   l_run += psum;
 }
 
