@@ -203,7 +203,7 @@ struct TileLoader {
   // an m0 write.
   __device__ void issue(const TileReq& q, uint32_t lds_rows, int u) const {
     constexpr int RB = D * 2;
-    const uint32_t lds = lds_rows + u * RPI * RB;
+    const uint32_t lds = __builtin_amdgcn_readfirstlane(lds_rows + u * RPI * RB);  // uniform; m0 takes an SGPR
     if constexpr (LAYOUT == PLayout::kPagedFine) {
       const int t = fine_key(q.t0, u);
       const int64_t off = static_cast<int64_t>(q.pg.fine[u]) * stride_page + static_cast<int64_t>(t & page_mask) * stride_token +
