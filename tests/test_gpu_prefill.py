@@ -130,6 +130,40 @@ def test_zero_query_gives_mean_over_visible_prefix():
         assert np.abs(lse[i] - np.log(n)).max() <= 1e-5
 
 
+@pytest.mark.parametrize("D", [64, 128])
+def test_tile_probability_sums_around_the_lazy_bound(D):
+    """Scores built so that the vector stage takes each of its paths: a tile whose probabilities against
+    the running maximum all stay below 1 (kept at the first try), a tile whose probabilities are about 8
+    each, so a lane's sum passes 2^8 while no probability does (taken again, no rescale), and a tile whose
+    scores jump by more than 8 in log2 units (taken again, rescaled). q is zero except head_dim 0, so a
+    key's score is q0 * K[t, hk, 0]: the value of K[., ., 0] per 64-key tile sets the pattern, in both
+    halves of the key tiles (16 tiles, the last one partial and masked)."""
+    from workloads.synth import f32_to_bf16_bits
+
+    L, M = 1000, 40
+    spec = small_prefill_spec(PREFILL_WORKLOADS[1], [L], [M], seed=60)
+    spec = spec.__class__(spec.name, spec.kv.replace(head_dim=D), spec.new_tokens, spec.seed)
+    pw = generate_prefill(spec)
+    c = float(pw.kv.spec.scale) * np.log2(np.e)  # log2 units per unit of score
+    # Tile levels in log2 units, relative to the start: 0, +3.1 (kept after a second try), +12.5 (rescale),
+    # equal (kept), back to 0 (kept), +3.1 above the new maximum twice (second try), +14.5 (rescale).
+    levels = np.array([0.0, 3.1, 12.5, 12.5, 0.0, 15.6, 15.6, 27.0] * 2)
+    k0 = f32_to_bf16_bits((levels / c).astype(np.float32)).astype(np.uint16)
+    k0f = (k0.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+    assert 32 * 2.0 ** ((k0f[1] - k0f[0]) * c) > 256 > 2.0 ** ((k0f[1] - k0f[0]) * c)
+    assert 32 * 2.0 ** ((k0f[5] - k0f[2]) * c) > 256 > 2.0 ** ((k0f[5] - k0f[2]) * c)
+    assert (k0f[2] - k0f[1]) * c > 8 and (k0f[7] - k0f[5]) * c > 8
+    pw.q[:] = 0
+    pw.q[:, :, 0] = f32_to_bf16_bits(np.ones(1, np.float32))[0]
+    pw.kv.k[:L, :, 0] = k0[np.arange(L) // 64][:, None]
+    say(f"prefill case lazy-bound tiles D={D}")
+    dp = DevicePrefill(pw)
+    out, lse = run_prefill(dp, make_op(pw.kv.spec))
+    ro, rl = pa.reference(pw)
+    ra, _ = pa.reference(abs_values(pw))
+    check_prefill(out, lse, ro, rl, ra, f"lazy-bound tiles D={D}")
+
+
 def test_single_new_token_matches_decode():
     """M_b = 1 is a decode step: the prefill kernel agrees with the oracle and with the decode kernel."""
     lens = [1, 33, 700, 4097]
