@@ -65,7 +65,7 @@ def test_groups_and_head_dims(G, D):
     check_prefill(out, lse, ro, rl, ra, f"G={G} D={D}")
 
 
-@pytest.mark.parametrize("ps", [1, 8, 16, 64, 128])
+@pytest.mark.parametrize("ps", [1, 2, 4, 8, 16, 64, 128])
 def test_paged_with_poison(ps):
     spec = small_prefill_spec(PREFILL_WORKLOADS[3], RAGGED_L, RAGGED_M, seed=53 + ps, max_ctx_len=2176)
     spec = spec.__class__(spec.name, spec.kv.replace(page_size=ps), spec.new_tokens, spec.seed)
