@@ -531,10 +531,19 @@ __device__ void attend_split(const AttnParams& p, SplitSmem<D, LAYOUT>& sm, int 
   finalize_split<D>(p, sm.ws, b, hk, j, nsplit_b);
 }
 
-// One workgroup per (split, KV head, sequence); splits past a sequence's end exit.
+// One workgroup per (split, KV head, sequence); splits past a sequence's end
+// exit. The KV head varies fastest with the linear workgroup id, the order
+// in which workgroups are dealt to the XCDs (round robin): with 8 KV heads
+// all splits of a head run on one XCD, and the heads of a token range are
+// read side by side. The batch-1 32K step with K and V in two allocations
+// took 29.1 instead of 30.3 us (27.8 and 27.9 us with the recommended
+// placement).
 template <int D, Layout LAYOUT, bool FP8>
 __global__ __launch_bounds__(kThreads, 2) void decode_mfma_kernel(const AttnParams p) {
-  const int j = blockIdx.x, hk = blockIdx.y, b = blockIdx.z;
+  const int lin = blockIdx.x + gridDim.x * (blockIdx.y + gridDim.y * blockIdx.z);
+  const int hk = lin % gridDim.y;
+  const int j = (lin / gridDim.y) % gridDim.x;
+  const int b = lin / (gridDim.x * gridDim.y);
   int L;
   int64_t seq_row;
   load_sequence<LAYOUT>(p, b, L, seq_row);
