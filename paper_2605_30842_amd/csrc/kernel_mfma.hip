@@ -532,18 +532,22 @@ __device__ void attend_split(const AttnParams& p, SplitSmem<D, LAYOUT>& sm, int 
 }
 
 // One workgroup per (split, KV head, sequence); splits past a sequence's end
-// exit. The KV head varies fastest with the linear workgroup id, the order
-// in which workgroups are dealt to the XCDs (round robin): with 8 KV heads
-// all splits of a head run on one XCD, and the heads of a token range are
-// read side by side. The batch-1 32K step with K and V in two allocations
-// took 29.1 instead of 30.3 us (27.8 and 27.9 us with the recommended
-// placement).
+// exit. Within a sequence the KV head varies fastest with the linear
+// workgroup id, the order in which workgroups are dealt to the XCDs (round
+// robin): with 8 KV heads all splits of a head run on one XCD, and the heads
+// of a token range are read side by side. The batch-1 32K step with K and V
+// in two allocations took 29.1 instead of 30.3 us (27.8 and 27.9 us with the
+// recommended placement). Grids of more than 2^24 workgroups per sequence
+// keep the direct order (the 32-bit index arithmetic stays exact).
 template <int D, Layout LAYOUT, bool FP8>
 __global__ __launch_bounds__(kThreads, 2) void decode_mfma_kernel(const AttnParams p) {
-  const int lin = blockIdx.x + gridDim.x * (blockIdx.y + gridDim.y * blockIdx.z);
-  const int hk = lin % gridDim.y;
-  const int j = (lin / gridDim.y) % gridDim.x;
-  const int b = lin / (gridDim.x * gridDim.y);
+  int j = blockIdx.x, hk = blockIdx.y;
+  const int b = blockIdx.z;
+  if (static_cast<uint64_t>(gridDim.x) * gridDim.y <= (1u << 24)) {
+    const uint32_t lin = blockIdx.x + gridDim.x * blockIdx.y;
+    hk = static_cast<int>(lin % gridDim.y);
+    j = static_cast<int>(lin / gridDim.y);
+  }
   int L;
   int64_t seq_row;
   load_sequence<LAYOUT>(p, b, L, seq_row);
