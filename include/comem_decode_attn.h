@@ -166,7 +166,7 @@ comem_status comem_decode_attn_device_errors(const comem_decode_attn_plan* plan,
  * V base lies COMEM_V_BASE_OFFSET_BYTES past the K base modulo
  * COMEM_V_BASE_OFFSET_MODULUS than when the two bases are congruent modulo
  * 512 (any two separate allocations of 4 KB granularity are): the batch-1
- * 32768-token bf16 step takes 27.8-28.0 instead of 29.5-30.1 us (depending
+ * 32768-token bf16 step takes 27.7-28.0 instead of 29.0-29.2 us (depending
  * on the device), its FP8 form 18.9 instead of 20.7 us, and multi-GB batches
  * are 0.7-1.4% faster. Differences
  * of 256, 768, 1280, 1792 and 2304 bytes all give the faster time; 0, 1024,
