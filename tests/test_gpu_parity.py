@@ -70,6 +70,16 @@ def test_groups_and_head_dims(variant, G, D):
     check(out, lse, ro, rl, "bf16", f"G={G} D={D} {variant}")
 
 
+@pytest.mark.parametrize("variant", ["mfma", "mfma_grid"])
+@pytest.mark.parametrize("hkv", [1, 3, 5, 8, 12])
+def test_kv_head_counts(variant, hkv):
+    """KV head counts that do and do not divide the 8 XCDs: the grid form orders its workgroups
+    head-major within a sequence, so every (split, head) pair must still be run exactly once."""
+    spec = small_spec(WORKLOADS[2], [1, 700, 3000], seed=40 + hkv).replace(num_q_heads=2 * hkv, num_kv_heads=hkv)
+    _, _, _, out, lse, ro, rl = _case(spec, variant=variant, chunk=128)
+    check(out, lse, ro, rl, "bf16", f"Hkv={hkv} {variant}")
+
+
 @pytest.mark.parametrize("G,D", [(4, 64), (8, 128), (16, 64)])
 def test_fp32_groups(G, D):
     spec = small_spec(WORKLOADS[1], [3, 200], seed=24).replace(num_q_heads=2 * G, num_kv_heads=2, head_dim=D)
