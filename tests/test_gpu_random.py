@@ -8,8 +8,12 @@ checked element by element against the oracle with the same gates as the
 other parity tests: decode attention, decode with the fused append (cache
 bits against the oracle's append, output bits against the separate calls)
 and prefill over a cached prefix. The sizes keep the whole sweep under a
-minute on one GPU.
+minute on one GPU; the environment variables COMEM_RANDOM_DECODE_CASES,
+COMEM_RANDOM_PREFILL_CASES, COMEM_RANDOM_APPEND_CASES and
+COMEM_RANDOM_QUEUE_CASES set larger counts for longer sweeps.
 """
+
+import os
 
 import numpy as np
 import pytest
@@ -22,7 +26,7 @@ pytestmark = pytest.mark.gpu
 
 VARIANTS = {"f32": ["auto", "valu"], "bf16": ["auto", "mfma", "mfma_grid", "valu"], "fp8": ["auto", "mfma", "mfma_grid"]}
 BASE = {("f32", False): 1, ("bf16", False): 2, ("bf16", True): 4, ("fp8", False): 6, ("fp8", True): 7}
-NUM_CASES = 160
+NUM_CASES = int(os.environ.get("COMEM_RANDOM_DECODE_CASES", 160))
 
 
 def draw_case(i: int) -> dict:
@@ -77,7 +81,7 @@ def test_random_case_matches_the_oracle(i):
     check(out, lse, ro, rl, c["dtype"], f"random case {i}")
 
 
-NUM_PREFILL_CASES = 64
+NUM_PREFILL_CASES = int(os.environ.get("COMEM_RANDOM_PREFILL_CASES", 64))
 
 
 def draw_prefill_case(i: int) -> dict:
@@ -119,7 +123,7 @@ def test_random_prefill_case_matches_the_oracle(i):
     check_prefill(out, lse, ro, rl, ra, f"random prefill case {i}")
 
 
-NUM_APPEND_CASES = 48
+NUM_APPEND_CASES = int(os.environ.get("COMEM_RANDOM_APPEND_CASES", 48))
 
 
 @pytest.mark.parametrize("i", range(NUM_APPEND_CASES))
@@ -163,7 +167,7 @@ def test_random_fused_append_case(i):
     check(out.cpu().numpy(), lse.cpu().numpy(), ro, rl, spec.dtype, f"random fused append case {i}")
 
 
-NUM_QUEUE_CASES = 12
+NUM_QUEUE_CASES = int(os.environ.get("COMEM_RANDOM_QUEUE_CASES", 12))
 
 
 def draw_queue_case(i: int) -> dict:
