@@ -46,7 +46,9 @@
 //
 // The running maximum moves lazily: it is raised only when a row's new
 // maximum exceeds it by more than 2^8 in probability, so the accumulators are
-// rescaled rarely and every probability stays below 2^8.
+// rescaled rarely and every probability stays below 2^8. A tile's
+// probabilities are first taken against the running maximum as it is; the
+// tile's own maximum is computed only when a lane's sum of them passes 2^8.
 //
 // K and V tiles go from global memory straight into LDS (buffer loads with an
 // LDS destination), K two tiles and V one tile ahead of the compute, into two
@@ -57,7 +59,7 @@
 // the K reads (one chunk of 8 or 16 consecutive rows), the V transpose reads
 // (4 chunks of 4 consecutive rows) and the stores are all free of bank
 // conflicts. Paged caches look their block-table entries up ahead of the
-// requests.
+// requests (scalar loads for pages of 16 rows or more).
 #include "attn_common.h"
 #include "prefill.h"
 
