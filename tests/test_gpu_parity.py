@@ -204,6 +204,24 @@ def test_fused_kv_buffer_strides(variant):
     check(out, lse, ro, rl, "bf16", f"fused kv {variant}")
 
 
+@pytest.mark.parametrize("variant", ["mfma", "mfma_grid", "valu"])
+def test_head_major_cache_strides(variant):
+    """K and V stored head-major ([Hkv, T, D] per tensor) and passed as [T, Hkv, D] views
+    (stride_token = D, stride_head = T * D): the same bits as the token-major cache."""
+    spec = small_spec(WORKLOADS[2], [300, 1, 2100, 0, 129], seed=35)
+    w = generate(spec)
+    dw = DeviceWorkload(w)
+    op = make_op(spec, variant=variant, chunk=128)
+    say(f"case head-major cache {variant}")
+    want = run(dw, op)
+    dw.k = dw.k.permute(1, 0, 2).contiguous().permute(1, 0, 2)
+    dw.v = dw.v.permute(1, 0, 2).contiguous().permute(1, 0, 2)
+    assert dw.k.stride() == (spec.head_dim, dw.k.shape[0] * spec.head_dim, 1)
+    got = run(dw, op)
+    assert np.array_equal(want[0], got[0]) and np.array_equal(want[1], got[1])
+    check(got[0], got[1], *da.reference(w), "bf16", f"head-major {variant}")
+
+
 def test_workspace_reused_across_changing_calls():
     """Ticket counters return to zero: calls with different split counts share one workspace."""
     base = small_spec(WORKLOADS[2], [2000], seed=33, max_ctx_len=8192)
