@@ -692,6 +692,64 @@ def _read_ceiling(nbytes, steps, blocks=4096):
             "buffers_cycled": copies}
 
 
+def _read_kv_heads(spec, tokens, chunk, placement, steps):
+    """A bare read of the headline cache with the decode kernel's grid and per-lane loads
+    (comem_probe_read_kv_heads), timed like the decode steps (graph replays, cycling over KV copies placed
+    as in the decode measurement): the ceiling of the kernel's access pattern. None where it does not apply
+    (paged or ragged caches, head_dim other than 128, fp32, or lengths not a multiple of the split)."""
+    import torch
+
+    from paper_2605_30842_amd import binding
+
+    head_bytes = {"bf16": 256, "fp8": 128}.get(spec.dtype)
+    if (spec.layout != "contiguous" or spec.batch != 1 or spec.head_dim != 128 or head_bytes is None or
+            tokens % chunk != 0 or chunk % 128 != 0):
+        return None
+    binding.load_probe_library()
+    dev = torch.device("cuda:0")
+    shape = (tokens, spec.num_kv_heads, spec.head_dim)
+    dtype = torch.bfloat16 if spec.dtype == "bf16" else torch.uint8
+    kv_bytes = 2 * tokens * spec.num_kv_heads * head_bytes
+    copies = max(1, math.ceil(4 * MALL_BYTES / kv_bytes))
+    kv = []
+    for _ in range(copies):
+        if placement == "offset":
+            kc, vc = binding.kv_cache_pair(shape, dtype, dev)
+        else:
+            kc, vc = torch.empty(shape, dtype=dtype, device=dev), torch.empty(shape, dtype=dtype, device=dev)
+        kc.view(torch.uint8).fill_(1)
+        vc.view(torch.uint8).fill_(1)
+        kv.append((kc, vc))
+    sink = torch.zeros(256, dtype=torch.int32, device=dev)
+    stride = spec.num_kv_heads * head_bytes
+    per_graph = copies * max(1, -(-16 // copies))
+    stream = torch.cuda.current_stream()
+    g = torch.cuda.CUDAGraph()
+    side = torch.cuda.Stream()
+    side.wait_stream(stream)
+    with torch.cuda.graph(g, stream=side):
+        for i in range(per_graph):
+            kc, vc = kv[i % copies]
+            binding.comem_probe_read_kv_heads(kc.data_ptr(), vc.data_ptr(), tokens, spec.num_kv_heads, head_bytes,
+                                              stride, chunk, sink.data_ptr(), torch.cuda.current_stream().cuda_stream)
+    torch.cuda.synchronize()
+    reps = max(1, steps // per_graph)
+    g.replay()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(reps):
+        g.replay()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    us = e0.elapsed_time(e1) * 1e3 / (reps * per_graph)
+    del kv, sink, g
+    torch.cuda.empty_cache()
+    return {"bytes": kv_bytes, "split_tokens": chunk, "kv_placement": placement, "us_per_call": round(us, 3),
+            "GBps": round(kv_bytes / (us * 1e-6) / 1e9, 1),
+            "frac_of_peak": round(kv_bytes / (us * 1e-6) / 1e9 / PEAK_HBM_GBPS, 4), "buffers_cycled": copies}
+
+
 def _summary(r):
     gbps = r["kv_bytes"] / (r["ms"] * 1e-3) / 1e9
     d = {"us_per_step": round(r["ms"] * 1e3, 3), "GBps": round(gbps, 1), "frac_of_peak": round(gbps / PEAK_HBM_GBPS, 4),
@@ -765,6 +823,9 @@ def main():
             also[rw["spec"].name] = dict(_summary(rw), kv_placement=a.kv_placement)
             print(f"# {rw['spec'].name}: {rw['ms'] * 1e3:.3f} us/step", file=sys.stderr, flush=True)
         ceiling = {"read_4GiB": _read_ceiling(4 << 30, 160), "read_same_bytes": _read_ceiling(kv_bytes, a.steps)}
+        pattern = _read_kv_heads(spec, int(r["ctx_len_total"]), r["chunk"], a.kv_placement, a.steps)
+        if pattern is not None:
+            ceiling["read_kernel_pattern"] = pattern
         print(f"# read ceiling: {ceiling}", file=sys.stderr, flush=True)
 
     kind = a.variant if a.variant != "auto" else ("valu" if spec.dtype == "f32" else "mfma")

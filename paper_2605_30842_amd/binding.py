@@ -36,7 +36,7 @@ EXPORTED = (
 NOALLOC_SCRATCH_BYTES = 32 << 20  # COMEM_NOALLOC_SCRATCH_BYTES
 FLAG_DEBUG_CHECKS = 1
 DEVICE_ERR_CTX_LEN, DEVICE_ERR_BLOCK_TABLE = 1, 2
-PROBE_EXPORTED = ("comem_probe_read", "comem_probe_copy")
+PROBE_EXPORTED = ("comem_probe_read", "comem_probe_copy", "comem_probe_read_kv_heads")
 COST_EXPORTED = (
     "comem_cost_kv_bytes_per_token", "comem_cost_decode_time", "comem_cost_decode_saving",
     "comem_cost_prefill_time", "comem_cost_net_saving", "comem_cost_max_compression_ratio",
@@ -166,6 +166,9 @@ def load_probe_library(path: str = PROBE_LIB_PATH) -> ctypes.CDLL:
     lib.comem_probe_read.restype = ctypes.c_int
     lib.comem_probe_copy.argtypes = [vp, vp, sz, ctypes.c_int, vp]
     lib.comem_probe_copy.restype = ctypes.c_int
+    i32, i64 = ctypes.c_int32, ctypes.c_int64
+    lib.comem_probe_read_kv_heads.argtypes = [vp, vp, i64, i32, i32, i64, i32, vp, vp]
+    lib.comem_probe_read_kv_heads.restype = ctypes.c_int
     _probe = lib
     return lib
 
@@ -180,6 +183,13 @@ def comem_probe_copy(src, dst, nbytes, blocks, stream) -> None:
     err = load_probe_library().comem_probe_copy(src, dst, nbytes, blocks, stream)
     if err != 0:
         raise RuntimeError(f"comem_probe_copy: HIP error {err}")
+
+
+def comem_probe_read_kv_heads(k, v, tokens, kv_heads, head_bytes, stride_token, chunk, sink, stream) -> None:
+    err = load_probe_library().comem_probe_read_kv_heads(k, v, tokens, kv_heads, head_bytes, stride_token, chunk,
+                                                         sink, stream)
+    if err != 0:
+        raise RuntimeError(f"comem_probe_read_kv_heads: HIP error {err}")
 
 
 def status_string(status: int) -> str:

@@ -46,6 +46,23 @@ def test_probe_library_exports_its_header():
         assert hasattr(lib, name), name
 
 
+def test_probe_read_kv_heads_rejects_bad_arguments():
+    """Every argument rule of the pattern-read probe is checked on the host, before any launch
+    (hipErrorInvalidValue = 1); the pointers are never dereferenced on the host."""
+    lib = B.load_probe_library()
+    k, v, sink = 1 << 20, 2 << 20, 3 << 20
+    good = dict(k=k, v=v, tokens=32768, kv_heads=8, head_bytes=256, stride_token=2048, chunk=1024, sink=sink)
+    bad = [dict(k=0), dict(v=0), dict(sink=0), dict(head_bytes=64), dict(head_bytes=512), dict(chunk=0),
+           dict(chunk=96), dict(tokens=0), dict(tokens=1000), dict(kv_heads=0), dict(stride_token=1024),
+           dict(stride_token=2056), dict(k=k + 8), dict(v=v + 4), dict(kv_heads=70000, stride_token=70000 * 256),
+           dict(tokens=1 << 31, chunk=128, kv_heads=2, stride_token=512)]
+    for change in bad:
+        a = dict(good, **change)
+        st = lib.comem_probe_read_kv_heads(a["k"], a["v"], a["tokens"], a["kv_heads"], a["head_bytes"],
+                                           a["stride_token"], a["chunk"], a["sink"], None)
+        assert st == 1, change
+
+
 def _cfg(**kw):
     base = dict(num_q_heads=32, num_kv_heads=8, head_dim=128, dtype=B.BF16, scale=0.088, max_batch=4,
                 max_ctx_len=4096, chunk_tokens=0, variant=B.VARIANT_AUTO, k_scale=1.0, v_scale=1.0)
