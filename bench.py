@@ -14,8 +14,10 @@ oracle timed on a bounded sample as a reported baseline. The same run also
 times, with the same rules, the headline workload with its K and V caches in
 the other placement, the other workloads of the 32k-128k range (batch 16
 ragged up to 64K, batch 64 paged, batch 8 at 128K), and a streaming read of
-4 GiB and of the headline's byte count (the practical read ceiling); those
-go under config.also and roofline.read_ceiling (--no-also skips them).
+4 GiB and of the headline's byte count (the practical read ceiling), and a
+bare read of the headline's cache with the kernel's grid and per-lane loads
+(the ceiling of its access pattern); those go under config.also and
+roofline.read_ceiling (--no-also skips them).
 """
 
 from __future__ import annotations
